@@ -1,0 +1,224 @@
+"""Plain CPU oracle of the GNMR controller pass (float64, NumPy).
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py may import or call this module.  The product
+path (the HIP library and its Python binding) never does, and this module
+imports nothing from it.
+
+What it computes, per controller step t = 1, 2, ... (paper notation):
+
+  norm    n_{b,t} = ||g_{b,t}||_2 over all parameters of unit b; a unit made
+          of several tensors is the L2 norm of their concatenation
+          (Sec. 2, local-gradient equation; Sec. 3.4, block as unit).
+  GNMR    1 if t = 1 or A_{b,t-1} = 0, else n_{b,t} / (A_{b,t-1} + eps)
+          (Alg. 1; GNMR definition of Sec. 3.1).
+  D-GNMR  GNMR_{b,t} / (mean(Q_b) + eps) once Q_b holds delta values, else 1;
+          Q_b holds the delta previous GNMR values, the current one excluded
+          (Alg. 1; Delta-GNMR definition of Sec. 3.2).
+  state   A_{b,t} = A_{b,t-1} + (n_{b,t} - A_{b,t-1}) / t, then push GNMR_{b,t}
+          into Q_b and keep the newest delta values (Alg. 1).
+  risk    R_{b,t} = max(GNMR_{b,t} / alpha_t, D-GNMR_{b,t} / beta_t)
+          (Alg. 2; Sec. 3.3).
+  pool    C_t = {b : R_{b,t} > 1} U {b : Lock_b > 0}, recoverable units only,
+          Lock_b as left by step t-1 (Alg. 2; Sec. 3.3).
+  select  A_t = Top_maxO(C_t; R): all of C_t when |C_t| <= maxO, else the
+          maxO members with the largest R; maxO caps the active set, it is not
+          a quota (Alg. 2; Sec. 3.4; App. E matched-trigger setting).
+  locks   b in A_t and R > 1 -> Lock_b = T_lock; b in A_t and R <= 1 ->
+          Lock_b = max(Lock_b - 1, 0); b not in A_t -> Lock_b = 0 (Alg. 2).
+
+Readings where the paper is silent (each also listed in the design doc):
+  * Ties in Top_maxO are broken by the smaller unit index.
+  * eps = 0 with a zero D-GNMR denominator gives D-GNMR = 1 (the same
+    convention Alg. 1 uses for A = 0).
+  * t is the global controller step; every step is an observation, n = 0
+    included.
+  * Non-finite n (outside the paper): GNMR = D-GNMR = R = +inf, A_b kept,
+    1.0 pushed into Q_b, counted in n_nonfinite.
+  * Statistics: n_trig_gnmr = #{GNMR/alpha > 1}, n_trig_dgnmr =
+    #{D-GNMR/beta > 1}, n_trig = #{R > 1}, all over recoverable units;
+    hit_maxo = 1 when |C_t| >= maxO and C_t is non-empty.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+
+F32 = 0
+BF16 = 1
+
+
+# --------------------------------------------------------------------------
+# norm  (Sec. 2, local-gradient equation)
+# --------------------------------------------------------------------------
+
+def widen(values: np.ndarray, dtype: int) -> np.ndarray:
+    """Exact widening to float64.  bf16 is given as uint16 bit patterns."""
+    if dtype == F32:
+        return np.asarray(values, dtype=np.float32).astype(np.float64)
+    if dtype == BF16:
+        bits = np.asarray(values, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return bits.view(np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype}")
+
+
+def sumsq(segments, chunk: int = 1 << 22) -> float:
+    """Sum of squares over a unit's segments, each a (values, dtype) pair.
+
+    Every square of a widened bf16 or fp32 value is exact in float64; only
+    the summation rounds."""
+    s = 0.0
+    for values, dtype in segments:
+        values = np.asarray(values).reshape(-1)
+        for lo in range(0, values.size, chunk):
+            x = widen(values[lo:lo + chunk], dtype)
+            s += float(np.dot(x, x))
+    return s
+
+
+def unit_norm(segments) -> float:
+    return math.sqrt(sumsq(segments))
+
+
+# --------------------------------------------------------------------------
+# controller state and one step  (Alg. 1 and Alg. 2)
+# --------------------------------------------------------------------------
+
+@dataclass
+class StepResult:
+    t: int
+    norm: np.ndarray
+    gnmr: np.ndarray
+    dgnmr: np.ndarray
+    risk: np.ndarray
+    mask: np.ndarray      # uint8, 1 = recovery path this step (b in A_t)
+    lock: np.ndarray      # int32, Lock_b after the step
+    stats: dict
+
+
+class Controller:
+    """Per-unit GNMR state: step counter t, historical means A_b, recent
+    GNMR queues Q_b (length <= delta), lock counters Lock_b."""
+
+    def __init__(self, num_units: int, window: int, max_o: int, lock_len: int,
+                 eps: float, recoverable=None):
+        if num_units < 1 or window < 1 or max_o < 0 or lock_len < 0:
+            raise ValueError("need num_units >= 1, window >= 1, max_o >= 0, lock_len >= 0")
+        if not (eps >= 0.0 and math.isfinite(eps)):
+            raise ValueError("need finite eps >= 0")
+        self.U = int(num_units)
+        self.delta = int(window)
+        self.max_o = int(max_o)
+        self.lock_len = int(lock_len)
+        self.eps = float(eps)
+        if recoverable is None:
+            self.rec = np.ones(self.U, dtype=bool)
+        else:
+            self.rec = np.asarray(recoverable).astype(bool).reshape(-1)
+            if self.rec.size != self.U:
+                raise ValueError("recoverable must have num_units entries")
+        self.t = 0                                   # steps taken so far
+        self.A = np.zeros(self.U)                    # historical means A_b
+        self.Q: list[np.ndarray] = []                # oldest first, each [U]
+        self.lock = np.zeros(self.U, dtype=np.int64)
+
+    # -- state snapshot -----------------------------------------------------
+    def get_state(self) -> dict:
+        return {"t": self.t, "A": self.A.copy(), "Q": [q.copy() for q in self.Q],
+                "lock": self.lock.copy()}
+
+    def set_state(self, st: dict) -> None:
+        self.t = int(st["t"])
+        self.A = np.array(st["A"], dtype=np.float64)
+        self.Q = [np.array(q, dtype=np.float64) for q in st["Q"]]
+        self.lock = np.array(st["lock"], dtype=np.int64)
+
+    # -- one controller step --------------------------------------------------
+    def step(self, norms, alpha: float, beta: float) -> StepResult:
+        if not (alpha > 0 and beta > 0 and math.isfinite(alpha) and math.isfinite(beta)):
+            raise ValueError("thresholds must be finite and > 0")
+        n = np.asarray(norms, dtype=np.float64).reshape(-1)
+        if n.size != self.U:
+            raise ValueError("one norm per unit expected")
+        U, delta, eps = self.U, self.delta, self.eps
+        t = self.t + 1
+        finite = np.isfinite(n)
+
+        # Alg. 1: GNMR = 1 at t = 1 or when the historical mean is 0.
+        gnmr = np.ones(U)
+        if t > 1:
+            has_mean = finite & (self.A != 0.0)
+            gnmr[has_mean] = n[has_mean] / (self.A[has_mean] + eps)
+
+        # Alg. 1: Delta-GNMR against the mean of the delta previous GNMRs.
+        dgnmr = np.ones(U)
+        if len(self.Q) == delta:
+            total = np.zeros(U)
+            for q in self.Q:                       # oldest to newest
+                total = total + q
+            den = total / delta + eps
+            ok = finite & (den != 0.0)
+            dgnmr[ok] = gnmr[ok] / den[ok]
+
+        # Alg. 1: running mean and queue push.
+        A_next = self.A + (n - self.A) / t
+        self.A = np.where(finite, A_next, self.A)
+        pushed = np.where(finite, gnmr, 1.0)
+        self.Q.append(pushed)
+        if len(self.Q) > delta:
+            self.Q.pop(0)
+
+        gnmr = np.where(finite, gnmr, np.inf)
+        dgnmr = np.where(finite, dgnmr, np.inf)
+
+        # Alg. 2: combined risk.
+        g_term = gnmr / alpha
+        d_term = dgnmr / beta
+        risk = np.maximum(g_term, d_term)
+
+        # Alg. 2: candidate pool (lock counters from the previous step).
+        triggered = self.rec & (risk > 1.0)
+        cand = triggered | (self.rec & (self.lock > 0))
+        cand_idx = np.flatnonzero(cand)
+
+        # Alg. 2: Top_maxO by R, ties to the smaller index.
+        if cand_idx.size <= self.max_o:
+            active = cand_idx
+        else:
+            order = np.lexsort((cand_idx, -risk[cand_idx]))
+            active = cand_idx[order[: self.max_o]]
+        mask = np.zeros(U, dtype=np.uint8)
+        mask[active] = 1
+
+        # Alg. 2: lock update.
+        new_lock = np.zeros(U, dtype=np.int64)
+        for b in active:
+            if risk[b] > 1.0:
+                new_lock[b] = self.lock_len
+            else:
+                new_lock[b] = max(self.lock[b] - 1, 0)
+        self.lock = new_lock
+        self.t = t
+
+        stats = {
+            "t": t,
+            "n_trig_gnmr": int(np.count_nonzero(self.rec & (g_term > 1.0))),
+            "n_trig_dgnmr": int(np.count_nonzero(self.rec & (d_term > 1.0))),
+            "n_trig": int(np.count_nonzero(triggered)),
+            "n_cand": int(cand_idx.size),
+            "n_active": int(active.size),
+            "hit_maxo": int(cand_idx.size > 0 and cand_idx.size >= self.max_o),
+            "n_nonfinite": int(np.count_nonzero(~finite)),
+        }
+        return StepResult(t, n.copy(), gnmr, dgnmr, risk, mask,
+                          self.lock.astype(np.int32), stats)
+
+
+def run_stream(norms_by_step, alphas, betas, **cfg) -> list[StepResult]:
+    """Run a controller over a [T, U] norm stream."""
+    norms_by_step = np.asarray(norms_by_step, dtype=np.float64)
+    ctl = Controller(norms_by_step.shape[1], **cfg)
+    return [ctl.step(norms_by_step[i], alphas[i], betas[i])
+            for i in range(norms_by_step.shape[0])]
