@@ -1,0 +1,162 @@
+"""Benchmark of the GNMR controller pass on one MI355X.
+
+One step = one gnmr_step: the gradient pass over every unit (K1), the
+Alg. 1 state update and risk (K2) and the Top_maxO selection with locks (K3),
+over gradients already resident in HBM.  The default workload is the
+LLaMA-2-13B-shaped bf16 gradient set (280 units, 25.38 GB per step).
+
+Prints one JSON line: whole-step GB/s (algorithmic bytes = every gradient
+byte once), ms and us per step, the dominant kernel's roofline position, and
+the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "GNMR step GB/s (frac. of HBM peak) + µs/step, 13B-shaped grads, 1 GPU"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(torch, buf, lay, w, target_s: float = 10.0, max_units: int = 64):
+    """Oracle norm pass plus one oracle controller step, single-threaded, on a
+    bounded sample of units copied off the device (copy not timed)."""
+    import numpy as np
+
+    from oracle import Controller as Oracle
+    from oracle import sumsq
+
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:                                  # pragma: no cover
+        limiter = None
+    order = np.random.default_rng(0).permutation(w.num_units)
+    spent, nbytes, units = 0.0, 0, 0
+    for b in order[:max_units]:
+        s = int(lay.seg_byte_off[b])
+        n = int(lay.seg_numel[b])
+        esz = 2 if int(lay.seg_dtype[b]) == 1 else 4
+        host = buf[s:s + n * esz].cpu().numpy()
+        vals = host.view(np.uint16) if esz == 2 else host.view(np.float32)
+        t0 = time.perf_counter()
+        sumsq([(vals, int(lay.seg_dtype[b]))])
+        spent += time.perf_counter() - t0
+        nbytes += n * esz
+        units += 1
+        if spent >= target_s:
+            break
+    ora = Oracle(w.num_units, window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=w.eps)
+    norms = np.ones(w.num_units)
+    t0 = time.perf_counter()
+    ora.step(norms, w.alpha(1), w.beta(1))
+    logic_s = time.perf_counter() - t0
+    if limiter is not None:
+        limiter.unregister()
+    gbs = nbytes / spent / 1e9
+    step_s = w.bytes_per_step / (nbytes / spent) + logic_s
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "us_per_step": round(step_s * 1e6, 1),
+            "sample": f"float64 NumPy oracle norm pass over {units} of {w.num_units} units "
+                      f"({nbytes / 1e9:.2f} GB, {spent:.1f} s) plus one oracle controller step "
+                      f"over all units; us_per_step extrapolated to the full "
+                      f"{w.bytes_per_step / 1e9:.2f} GB step"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama2-13b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the controller pass runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_00539_amd import Controller
+    from synth import layout as L
+    from synth import recipe as R
+    from synth.gpu import Generator
+
+    assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    torch.cuda.set_device(0)
+    w = R.get(args.workload)
+    lay = L.for_workload(w)
+    log(f"[bench] {w.name}: {w.num_units} units, {w.bytes_per_step / 1e9:.3f} GB/step")
+    buf = torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda")
+    base = buf.data_ptr()
+    ptrs = [base + int(o) for o in lay.seg_byte_off]
+    Generator().fill(lay, base, w.seed, 1, w.scale32(1))
+    stream = torch.cuda.current_stream()
+    ctl = Controller(w.num_units, w.window, w.max_o, w.lock_len, w.eps, lay.unit_seg_off,
+                     lay.seg_numel, lay.seg_dtype, ptrs, stream=stream)
+    info = ctl.info()
+    t = 0
+    for _ in range(args.warmup):
+        t += 1
+        ctl.step(w.alpha(t), w.beta(t), stream=stream)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} steps done")
+
+    ctl.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        t += 1
+        ctl.step(w.alpha(t), w.beta(t), stream=stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ctl.profile_read()
+    ctl.set_profiling(False)
+    out = ctl.query(stream=stream)
+    log(f"[bench] timed {args.steps} steps in {elapsed:.4f} s; stats {out['stats']}")
+
+    ms = elapsed * 1e3 / args.steps
+    gbs = w.bytes_per_step / (elapsed / args.steps) / 1e9
+    k1_ms = prof["ms_sumsq"] / max(prof["steps"], 1)
+    k1_gbs = w.bytes_per_step / (k1_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k1_sumsq", "kernel_ms": round(k1_ms, 4),
+                "update_ms": round(prof["ms_update"] / max(prof["steps"], 1), 4),
+                "select_ms": round(prof["ms_select"] / max(prof["steps"], 1), 4)}
+    result = {
+        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "us_per_step": round(ms * 1e3, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name} gradients: {w.description}",
+                   "units": w.num_units, "grad_dtype": "bf16" if w.dtypes[0] == 1 else "fp32",
+                   "bytes_per_step": w.bytes_per_step, "max_o": w.max_o,
+                   "lock_len": w.lock_len, "window": w.window,
+                   "work_items": info["num_items"], "item_bytes": info["item_bytes"],
+                   "launches_per_step": info["launches_per_step"]},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(torch, buf, lay, w)
+    ctl.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

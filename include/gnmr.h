@@ -1,0 +1,172 @@
+/*
+ * gnmr.h -- C ABI of libgnmr, the per-step GNMR controller pass on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * One controller step does, for every monitored unit b (paper notation):
+ *   n_{b,t}   = ||g_{b,t}||_2 over all of b's gradient tensors
+ *               (Sec. 2, local-gradient equation; Sec. 3.4: a whole block may
+ *               be one unit, so a unit may own several tensors),
+ *   GNMR, Delta-GNMR, A_{b,t}, Q_b   (Alg. 1; definitions of Sec. 3.1, 3.2),
+ *   R_{b,t} = max(GNMR/alpha_t, Delta-GNMR/beta_t)  (Alg. 2; Sec. 3.3),
+ *   C_t = {R > 1} U {Lock > 0}, A_t = Top_maxO(C_t; R), lock update
+ *               (Alg. 2; Sec. 3.3; Sec. 3.4: maxO is a hard cap on |A_t|).
+ *
+ * Conventions the paper leaves open, fixed here:
+ *   - Top_maxO breaks ties in R by the smaller unit index.
+ *   - t is the global step, starting at 1; every step is an observation.
+ *   - eps = 0 and a zero Delta-GNMR denominator give Delta-GNMR = 1.
+ *   - A non-finite n_{b,t} (outside the paper): GNMR = Delta-GNMR = R = +inf,
+ *     A_b is kept, 1.0 enters Q_b, and the unit is counted in n_nonfinite.
+ *   - Units that are monitored but not recoverable get n, GNMR, Delta-GNMR
+ *     and R, never enter C_t, and keep Lock = 0.
+ *
+ * Every call returns a gnmr_status; on an error nothing about the controller
+ * state has changed and gnmr_last_error() describes the problem.  Calls on
+ * one context must not overlap; different contexts are independent.
+ * `stream` arguments are hipStream_t values (NULL = the null stream).
+ * "device" pointers are HIP device (or managed) memory of the current device;
+ * "host" pointers are ordinary host memory.
+ */
+#ifndef GNMR_H
+#define GNMR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gnmr_ctx gnmr_ctx;
+
+typedef enum {
+  GNMR_OK = 0,
+  GNMR_E_INVALID = -1, /* bad argument; nothing changed                        */
+  GNMR_E_NOMEM = -2,   /* device or host allocation failed                      */
+  GNMR_E_HIP = -3,     /* a HIP runtime call failed                             */
+  GNMR_E_STATE = -4    /* call not valid in the context's current state          */
+} gnmr_status;
+
+/* element types of gradient segments */
+enum { GNMR_F32 = 0, GNMR_BF16 = 1 };
+
+/* Controller settings (Alg. 1 and Alg. 2 inputs that do not change per step). */
+typedef struct {
+  int32_t num_units;          /* |B| >= 1, monitored units                       */
+  int32_t window;             /* delta >= 1, Delta-GNMR window                    */
+  int32_t max_o;              /* maxO >= 0, cap on the active recovery set        */
+  int32_t lock_len;           /* T_lock >= 0                                      */
+  double eps;                 /* epsilon >= 0, finite                              */
+  const uint8_t* recoverable; /* host [num_units], nonzero = in B_rec; NULL = all */
+} gnmr_config;
+
+/* Gradient layout: unit b owns segments [unit_seg_off[b], unit_seg_off[b+1]).
+ * A segment is a contiguous run of seg_numel[s] elements of type seg_dtype[s]
+ * starting at device address seg_ptr[s], which must be aligned to the element
+ * size (any other alignment is accepted).  All arrays are host memory and are
+ * copied by gnmr_init; the caller may free them afterwards.  Segments may be
+ * empty (numel 0) and units may own no segment (their norm is 0). */
+typedef struct {
+  int64_t num_segments;          /* S >= 0                                       */
+  const int64_t* unit_seg_off;   /* host [num_units + 1], [0] = 0, non-decreasing,
+                                    [num_units] = S                              */
+  const int64_t* seg_numel;      /* host [S], >= 0                                */
+  const int32_t* seg_dtype;      /* host [S], GNMR_F32 or GNMR_BF16               */
+  const void* const* seg_ptr;    /* host [S] of device pointers, or NULL: then
+                                    every gnmr_step / gnmr_sumsq must pass them  */
+} gnmr_segments;
+
+/* Per-step counters (trigger sparsity, promotion and hit-maxO rates of the
+ * paper's trigger-overhead measurements).  Counts are over recoverable units,
+ * except n_nonfinite, which is over all units. */
+typedef struct {
+  int64_t t;             /* step just completed (1-based)                          */
+  int32_t n_trig_gnmr;   /* #{GNMR/alpha_t > 1}                                    */
+  int32_t n_trig_dgnmr;  /* #{Delta-GNMR/beta_t > 1}                               */
+  int32_t n_trig;        /* #{R > 1}                                               */
+  int32_t n_cand;        /* |C_t|                                                  */
+  int32_t n_active;      /* |A_t| <= maxO                                          */
+  int32_t hit_maxo;      /* 1 if C_t is non-empty and |C_t| >= maxO                */
+  int32_t n_nonfinite;   /* units with a non-finite norm                           */
+  int32_t reserved;
+} gnmr_stats;
+
+/* Create a controller: t = 0, A = 0, Q empty, Lock = 0 (the state before the
+ * first step of Alg. 1 / Alg. 2).  Allocates all device state (O(U * delta)
+ * doubles plus one float per 64 KiB work item) and builds the work list over
+ * the segments.  `stream` orders the initial clears.  *out receives the
+ * context, or NULL on error. */
+gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg,
+                      const gnmr_segments* segs, void* stream);
+
+/* Release every resource of the context (waits for its pending work).
+ * NULL is accepted and ignored. */
+gnmr_status gnmr_destroy(gnmr_ctx* ctx);
+
+/* One full controller step t -> t + 1 (Alg. 1 for every unit, then Alg. 2):
+ * reads every gradient byte once, then updates A, Q, Lock and the outputs.
+ * alpha_t, beta_t > 0 and finite (values below 1 are legal).  seg_ptr: host
+ * [S] of device pointers for this step, or NULL to reuse the last bound ones.
+ * Asynchronous: only enqueues work on `stream`.  The gradient buffers must
+ * stay valid and unmodified until that work is done. */
+gnmr_status gnmr_step(gnmr_ctx* ctx, double alpha_t, double beta_t,
+                      const void* const* seg_ptr, void* stream);
+
+/* The same step with the norms given: d_norm is device [num_units] float64
+ * n_{b,t}; the gradient pass is skipped.  For callers that already hold the
+ * norms (and for testing the state update and selection alone). */
+gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm,
+                                 double alpha_t, double beta_t, void* stream);
+
+/* The gradient pass alone, without touching controller state: writes
+ * sum_i g_i^2 per unit (float64, device [num_units]) to d_sumsq.  seg_ptr as
+ * in gnmr_step.  Asynchronous. */
+gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
+                       double* d_sumsq, void* stream);
+
+/* Copy the last step's outputs to host memory; every destination may be NULL.
+ * Waits for `stream`.  Arrays are [num_units]: mask (1 = in A_t, recovery
+ * path), lock (Lock_b after the step), norm (n_{b,t}), gnmr, dgnmr, risk (R).
+ * GNMR_E_STATE before the first step. */
+gnmr_status gnmr_query(gnmr_ctx* ctx, uint8_t* mask, int32_t* lock, double* norm,
+                       double* gnmr, double* dgnmr, double* risk,
+                       gnmr_stats* stats, void* stream);
+
+/* Device addresses of the same outputs (owned by the context, valid until
+ * gnmr_destroy, overwritten by the next step).  Any pointer may be NULL. */
+gnmr_status gnmr_device_outputs(gnmr_ctx* ctx, const uint8_t** mask,
+                                const int32_t** lock, const double** norm,
+                                const double** gnmr, const double** dgnmr,
+                                const double** risk, const gnmr_stats** stats);
+
+/* Controller state (t, A, Q, Lock) as a flat, versioned byte blob, for
+ * checkpoint and resume.  gnmr_state_size gives the blob size; get copies it
+ * to host `buf` of `bytes` >= that size (waits for `stream`); set restores a
+ * blob taken from a context with the same num_units and window.  Restoring and
+ * then stepping reproduces the original run bit for bit. */
+gnmr_status gnmr_state_size(const gnmr_ctx* ctx, size_t* bytes);
+gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream);
+gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* stream);
+
+/* Kernel timing.  While enabled, every step records HIP events around each of
+ * its kernels on its stream.  gnmr_profile_read waits for them and returns the
+ * summed milliseconds of the gradient pass, the state update and the
+ * selection kernels over the steps recorded since enabling, and that number of
+ * steps; any output may be NULL.  Enabling resets the sums. */
+gnmr_status gnmr_set_profiling(gnmr_ctx* ctx, int enable);
+gnmr_status gnmr_profile_read(gnmr_ctx* ctx, double* ms_sumsq, double* ms_update,
+                              double* ms_select, int64_t* steps);
+
+/* Work-list facts: K1 work items, bytes per item, gradient bytes per step and
+ * kernel launches per gnmr_step.  Any output may be NULL. */
+gnmr_status gnmr_info(const gnmr_ctx* ctx, int64_t* num_items, int64_t* item_bytes,
+                      int64_t* bytes_per_step, int32_t* launches_per_step);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* gnmr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GNMR_H */

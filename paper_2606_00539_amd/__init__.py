@@ -1,0 +1,13 @@
+"""GNMR controller pass on AMD Instinct MI355X (gfx950).
+
+The controller pass (per-unit gradient L2 norms, GNMR / Delta-GNMR state
+update, budgeted Top_maxO selection with lock counters) runs in hand-written
+HIP kernels behind the C ABI of include/gnmr.h (libgnmr.so).  This package is
+the thin Python binding over that ABI.
+"""
+from .binding import (GNMR_BF16, GNMR_F32, Controller, GnmrError,  # noqa: F401
+                      gnmr_destroy, gnmr_device_outputs, gnmr_get_state, gnmr_info,
+                      gnmr_init, gnmr_last_error, gnmr_profile_read, gnmr_query,
+                      gnmr_set_profiling, gnmr_set_state, gnmr_state_size, gnmr_step,
+                      gnmr_step_from_norms, gnmr_sumsq, load_library)
+from .schedule import two_stage_alpha  # noqa: F401

@@ -1,0 +1,69 @@
+// Internal declarations shared by the runtime and the kernels of libgnmr.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gnmr.h"
+
+namespace gnmr {
+
+// K1 geometry: a workgroup of 256 lanes reads one work item of 64 KiB with
+// 16 outstanding 16-byte loads per lane.
+constexpr int kK1Block = 256;
+constexpr int kK1Unroll = 16;
+constexpr int64_t kItemBytes = int64_t(kK1Block) * kK1Unroll * 16;
+
+// One work item: elements [e0, e0 + count) of segment `seg`.  Items are
+// ordered by unit, so the items of unit b are [unit_item_off[b],
+// unit_item_off[b+1]).
+struct Item {
+  int64_t e0;
+  int32_t seg;
+  int32_t count;
+};
+static_assert(sizeof(Item) == 16, "Item layout");
+
+// Per-unit flag bits written by K2 and read by K3.
+enum : uint8_t { kFlagTrigG = 1, kFlagTrigD = 2, kFlagNonFinite = 4 };
+
+struct UpdateArgs {
+  int32_t num_units;
+  int32_t window;      // delta
+  int32_t qlen;        // values in Q before this step (min(t-1, delta))
+  int32_t slot;        // ring slot of the oldest value == slot of the new value
+  int64_t t;           // this step, 1-based
+  double eps, alpha, beta;
+  const int64_t* unit_item_off;  // [U+1]
+  const float* partial;          // [items]
+  const double* ext_norm;        // [U] or nullptr
+  double* A;                     // [U]
+  double* Q;                     // [window][U]
+  double* norm;
+  double* gnmr;
+  double* dgnmr;
+  double* risk;
+  uint8_t* flags;
+};
+
+struct SelectArgs {
+  int32_t num_units;
+  int32_t max_o;
+  int32_t lock_len;
+  int64_t t;
+  const double* risk;
+  const uint8_t* flags;
+  const uint8_t* rec;
+  int32_t* lock;       // in: Lock after step t-1; out: after step t
+  uint8_t* mask;
+  gnmr_stats* stats;
+};
+
+hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,
+                        const int32_t* seg_dtype, float* partial, hipStream_t s);
+hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,
+                             int32_t num_units, double* out, hipStream_t s);
+hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, uint64_t* keys, hipStream_t s);
+
+}  // namespace gnmr

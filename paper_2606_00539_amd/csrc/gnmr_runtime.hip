@@ -1,0 +1,592 @@
+// Host runtime of libgnmr: context, argument checks, the K1 work list,
+// kernel launches, outputs, state blob and kernel timing.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <array>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "gnmr_internal.h"
+
+using gnmr::Item;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+gnmr_status fail(gnmr_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+#define GNMR_HIP(expr)                                                                 \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(GNMR_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));      \
+  } while (0)
+
+constexpr uint32_t kStateMagic = 0x524D4E47u;  // "GNMR"
+constexpr uint32_t kStateVersion = 1;
+constexpr int kProfileCapacity = 4096;
+
+struct StateHeader {
+  uint32_t magic;
+  uint32_t version;
+  int32_t num_units;
+  int32_t window;
+  int64_t t;
+  int32_t max_o;
+  int32_t lock_len;
+  double eps;
+};
+static_assert(sizeof(StateHeader) == 40, "state header layout");
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Makes the context's device current for the duration of a call.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) {
+      ok = false;
+      return;
+    }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+struct gnmr_ctx {
+  int device = 0;
+  int32_t U = 0, window = 0, max_o = 0, lock_len = 0;
+  double eps = 0.0;
+  int64_t S = 0;
+  std::vector<int64_t> seg_numel;
+  std::vector<int32_t> seg_dtype;
+  int64_t num_items = 0;
+  int64_t bytes_per_step = 0;
+  int64_t t = 0;               // steps completed
+  bool ptrs_bound = false;
+
+  void* arena = nullptr;
+  Item* d_items = nullptr;
+  int64_t* d_unit_item_off = nullptr;
+  const char** d_seg_base = nullptr;
+  int32_t* d_seg_dtype = nullptr;
+  uint8_t* d_rec = nullptr;
+  float* d_partial = nullptr;
+  double* d_A = nullptr;
+  double* d_Q = nullptr;
+  int32_t* d_lock = nullptr;
+  double* d_norm = nullptr;
+  double* d_gnmr = nullptr;
+  double* d_dgnmr = nullptr;
+  double* d_risk = nullptr;
+  uint8_t* d_flags = nullptr;
+  uint8_t* d_mask = nullptr;
+  uint64_t* d_keys = nullptr;
+  gnmr_stats* d_stats = nullptr;
+
+  // pinned staging for segment-pointer uploads; `upload_done` guards reuse
+  const void** h_ptr_stage = nullptr;
+  hipEvent_t upload_done = nullptr;
+  bool upload_pending = false;
+
+  bool prof = false;
+  std::vector<std::array<hipEvent_t, 4>> prof_ev;
+  int64_t prof_steps = 0;
+};
+
+namespace {
+
+gnmr_status check_thresholds(double alpha, double beta) {
+  if (!(alpha > 0.0) || !(beta > 0.0) || !isfinite(alpha) || !isfinite(beta))
+    return fail(GNMR_E_INVALID, "alpha_t and beta_t must be finite and > 0");
+  return GNMR_OK;
+}
+
+gnmr_status check_ptrs(const gnmr_ctx* c, const void* const* ptrs) {
+  for (int64_t s = 0; s < c->S; ++s) {
+    if (c->seg_numel[s] == 0) continue;
+    const uintptr_t p = reinterpret_cast<uintptr_t>(ptrs[s]);
+    const uintptr_t esz = c->seg_dtype[s] == GNMR_BF16 ? 2 : 4;
+    if (p == 0) return fail(GNMR_E_INVALID, "segment " + std::to_string(s) + ": NULL pointer");
+    if (p % esz != 0)
+      return fail(GNMR_E_INVALID,
+                  "segment " + std::to_string(s) + ": pointer not aligned to its element size");
+  }
+  return GNMR_OK;
+}
+
+// Copies this step's segment pointers to the device table on `st`.
+gnmr_status bind_ptrs(gnmr_ctx* c, const void* const* ptrs, hipStream_t st) {
+  if (ptrs == nullptr) {
+    if (!c->ptrs_bound && c->num_items > 0)
+      return fail(GNMR_E_INVALID, "no segment pointers bound: pass seg_ptr");
+    return GNMR_OK;
+  }
+  gnmr_status r = check_ptrs(c, ptrs);
+  if (r != GNMR_OK) return r;
+  if (c->S == 0) return GNMR_OK;
+  if (c->upload_pending) {
+    GNMR_HIP(hipEventSynchronize(c->upload_done));
+    c->upload_pending = false;
+  }
+  memcpy(c->h_ptr_stage, ptrs, size_t(c->S) * sizeof(void*));
+  GNMR_HIP(hipMemcpyAsync(c->d_seg_base, c->h_ptr_stage, size_t(c->S) * sizeof(void*),
+                          hipMemcpyHostToDevice, st));
+  GNMR_HIP(hipEventRecord(c->upload_done, st));
+  c->upload_pending = true;
+  c->ptrs_bound = true;
+  return GNMR_OK;
+}
+
+gnmr_status record(gnmr_ctx* c, int which, hipStream_t st) {
+  if (!c->prof || c->prof_steps >= kProfileCapacity) return GNMR_OK;
+  if (size_t(c->prof_steps) >= c->prof_ev.size()) {
+    std::array<hipEvent_t, 4> ev{};
+    for (auto& e : ev) GNMR_HIP(hipEventCreate(&e));
+    c->prof_ev.push_back(ev);
+  }
+  GNMR_HIP(hipEventRecord(c->prof_ev[size_t(c->prof_steps)][which], st));
+  return GNMR_OK;
+}
+
+// K2 + K3 for step t+1 (K1 already enqueued when ext_norm is null).
+gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha, double beta,
+                              hipStream_t st) {
+  const int64_t t = c->t + 1;
+  gnmr::UpdateArgs u{};
+  u.num_units = c->U;
+  u.window = c->window;
+  u.qlen = int32_t(std::min<int64_t>(t - 1, c->window));
+  u.slot = int32_t((t - 1) % c->window);
+  u.t = t;
+  u.eps = c->eps;
+  u.alpha = alpha;
+  u.beta = beta;
+  u.unit_item_off = c->d_unit_item_off;
+  u.partial = c->d_partial;
+  u.ext_norm = ext_norm;
+  u.A = c->d_A;
+  u.Q = c->d_Q;
+  u.norm = c->d_norm;
+  u.gnmr = c->d_gnmr;
+  u.dgnmr = c->d_dgnmr;
+  u.risk = c->d_risk;
+  u.flags = c->d_flags;
+  GNMR_HIP(gnmr::launch_update(u, st));
+  gnmr_status r = record(c, 2, st);
+  if (r != GNMR_OK) return r;
+
+  gnmr::SelectArgs s{};
+  s.num_units = c->U;
+  s.max_o = c->max_o;
+  s.lock_len = c->lock_len;
+  s.t = t;
+  s.risk = c->d_risk;
+  s.flags = c->d_flags;
+  s.rec = c->d_rec;
+  s.lock = c->d_lock;
+  s.mask = c->d_mask;
+  s.stats = c->d_stats;
+  GNMR_HIP(gnmr::launch_select(s, c->d_keys, st));
+  r = record(c, 3, st);
+  if (r != GNMR_OK) return r;
+  c->t = t;
+  if (c->prof && c->prof_steps < kProfileCapacity) ++c->prof_steps;
+  return GNMR_OK;
+}
+
+void release(gnmr_ctx* c) {
+  if (c == nullptr) return;
+  if (c->upload_done) (void)hipEventSynchronize(c->upload_done);
+  for (auto& ev : c->prof_ev)
+    for (auto e : ev)
+      if (e) (void)hipEventDestroy(e);
+  if (c->upload_done) (void)hipEventDestroy(c->upload_done);
+  if (c->h_ptr_stage) (void)hipHostFree(c->h_ptr_stage);
+  if (c->arena) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(c->arena);
+  }
+  delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gnmr_last_error(void) { return g_last_error.c_str(); }
+
+gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segments* segs,
+                      void* stream) {
+  if (out == nullptr) return fail(GNMR_E_INVALID, "out is NULL");
+  *out = nullptr;
+  if (cfg == nullptr || segs == nullptr) return fail(GNMR_E_INVALID, "cfg or segs is NULL");
+  if (cfg->num_units < 1) return fail(GNMR_E_INVALID, "num_units must be >= 1");
+  if (cfg->window < 1) return fail(GNMR_E_INVALID, "window must be >= 1");
+  if (cfg->max_o < 0) return fail(GNMR_E_INVALID, "max_o must be >= 0");
+  if (cfg->lock_len < 0) return fail(GNMR_E_INVALID, "lock_len must be >= 0");
+  if (!(cfg->eps >= 0.0) || !isfinite(cfg->eps))
+    return fail(GNMR_E_INVALID, "eps must be finite and >= 0");
+  const int64_t U = cfg->num_units, S = segs->num_segments;
+  if (S < 0 || S > INT32_MAX) return fail(GNMR_E_INVALID, "num_segments out of range");
+  if (segs->unit_seg_off == nullptr) return fail(GNMR_E_INVALID, "unit_seg_off is NULL");
+  if (S > 0 && (segs->seg_numel == nullptr || segs->seg_dtype == nullptr))
+    return fail(GNMR_E_INVALID, "seg_numel or seg_dtype is NULL");
+  if (segs->unit_seg_off[0] != 0 || segs->unit_seg_off[U] != S)
+    return fail(GNMR_E_INVALID, "unit_seg_off must start at 0 and end at num_segments");
+  for (int64_t b = 0; b < U; ++b)
+    if (segs->unit_seg_off[b + 1] < segs->unit_seg_off[b])
+      return fail(GNMR_E_INVALID, "unit_seg_off must be non-decreasing");
+  for (int64_t s = 0; s < S; ++s) {
+    if (segs->seg_numel[s] < 0) return fail(GNMR_E_INVALID, "negative seg_numel");
+    if (segs->seg_dtype[s] != GNMR_F32 && segs->seg_dtype[s] != GNMR_BF16)
+      return fail(GNMR_E_INVALID, "unknown seg_dtype " + std::to_string(segs->seg_dtype[s]));
+  }
+
+  gnmr_ctx* c = new (std::nothrow) gnmr_ctx;
+  if (c == nullptr) return fail(GNMR_E_NOMEM, "host allocation failed");
+  c->U = cfg->num_units;
+  c->window = cfg->window;
+  c->max_o = cfg->max_o;
+  c->lock_len = cfg->lock_len;
+  c->eps = cfg->eps;
+  c->S = S;
+  c->seg_numel.assign(segs->seg_numel, segs->seg_numel + S);
+  c->seg_dtype.assign(segs->seg_dtype, segs->seg_dtype + S);
+  if (segs->seg_ptr != nullptr) {
+    gnmr_status r = check_ptrs(c, segs->seg_ptr);
+    if (r != GNMR_OK) {
+      delete c;
+      return r;
+    }
+  }
+
+  // K1 work list: each segment cut into items of kItemBytes, in unit order.
+  std::vector<Item> items;
+  std::vector<int64_t> unit_item_off(size_t(U) + 1, 0);
+  for (int64_t b = 0; b < U; ++b) {
+    for (int64_t s = segs->unit_seg_off[b]; s < segs->unit_seg_off[b + 1]; ++s) {
+      const int64_t esz = c->seg_dtype[s] == GNMR_BF16 ? 2 : 4;
+      const int64_t per = gnmr::kItemBytes / esz;
+      c->bytes_per_step += c->seg_numel[s] * esz;
+      for (int64_t e0 = 0; e0 < c->seg_numel[s]; e0 += per)
+        items.push_back(Item{e0, int32_t(s), int32_t(std::min(per, c->seg_numel[s] - e0))});
+    }
+    unit_item_off[size_t(b) + 1] = int64_t(items.size());
+  }
+  c->num_items = int64_t(items.size());
+  if (c->num_items > int64_t(UINT32_MAX)) {
+    delete c;
+    return fail(GNMR_E_INVALID, "too many work items");
+  }
+
+  // One device arena for all state.
+  const size_t a = 256;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + std::max<size_t>(bytes, 1), a);
+    return o;
+  };
+  const size_t o_items = take(items.size() * sizeof(Item));
+  const size_t o_uoff = take((size_t(U) + 1) * sizeof(int64_t));
+  const size_t o_base = take(size_t(S) * sizeof(void*));
+  const size_t o_dt = take(size_t(S) * sizeof(int32_t));
+  const size_t o_rec = take(size_t(U));
+  const size_t o_part = take(items.size() * sizeof(float));
+  const size_t o_A = take(size_t(U) * sizeof(double));
+  const size_t o_Q = take(size_t(U) * size_t(cfg->window) * sizeof(double));
+  const size_t o_lock = take(size_t(U) * sizeof(int32_t));
+  const size_t o_norm = take(size_t(U) * sizeof(double));
+  const size_t o_g = take(size_t(U) * sizeof(double));
+  const size_t o_d = take(size_t(U) * sizeof(double));
+  const size_t o_r = take(size_t(U) * sizeof(double));
+  const size_t o_fl = take(size_t(U));
+  const size_t o_mask = take(size_t(U));
+  const size_t o_keys = take(size_t(U) * sizeof(uint64_t));
+  const size_t o_st = take(sizeof(gnmr_stats));
+  const size_t total = off;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  auto bail = [&](gnmr_status s, const std::string& m) {
+    release(c);
+    return fail(s, m);
+  };
+  if (hipGetDevice(&c->device) != hipSuccess) return bail(GNMR_E_HIP, "hipGetDevice failed");
+  if (hipMalloc(&c->arena, total) != hipSuccess) {
+    c->arena = nullptr;
+    return bail(GNMR_E_NOMEM, "hipMalloc of " + std::to_string(total) + " bytes failed");
+  }
+  char* base = static_cast<char*>(c->arena);
+  c->d_items = reinterpret_cast<Item*>(base + o_items);
+  c->d_unit_item_off = reinterpret_cast<int64_t*>(base + o_uoff);
+  c->d_seg_base = reinterpret_cast<const char**>(base + o_base);
+  c->d_seg_dtype = reinterpret_cast<int32_t*>(base + o_dt);
+  c->d_rec = reinterpret_cast<uint8_t*>(base + o_rec);
+  c->d_partial = reinterpret_cast<float*>(base + o_part);
+  c->d_A = reinterpret_cast<double*>(base + o_A);
+  c->d_Q = reinterpret_cast<double*>(base + o_Q);
+  c->d_lock = reinterpret_cast<int32_t*>(base + o_lock);
+  c->d_norm = reinterpret_cast<double*>(base + o_norm);
+  c->d_gnmr = reinterpret_cast<double*>(base + o_g);
+  c->d_dgnmr = reinterpret_cast<double*>(base + o_d);
+  c->d_risk = reinterpret_cast<double*>(base + o_r);
+  c->d_flags = reinterpret_cast<uint8_t*>(base + o_fl);
+  c->d_mask = reinterpret_cast<uint8_t*>(base + o_mask);
+  c->d_keys = reinterpret_cast<uint64_t*>(base + o_keys);
+  c->d_stats = reinterpret_cast<gnmr_stats*>(base + o_st);
+
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ptr_stage),
+                    std::max<size_t>(size_t(S), 1) * sizeof(void*), hipHostMallocDefault) !=
+      hipSuccess) {
+    c->h_ptr_stage = nullptr;
+    return bail(GNMR_E_NOMEM, "hipHostMalloc of the pointer staging buffer failed");
+  }
+  if (hipEventCreateWithFlags(&c->upload_done, hipEventDisableTiming) != hipSuccess) {
+    c->upload_done = nullptr;
+    return bail(GNMR_E_HIP, "hipEventCreate failed");
+  }
+
+  std::vector<uint8_t> rec(size_t(U), 1);
+  if (cfg->recoverable != nullptr)
+    for (int64_t b = 0; b < U; ++b) rec[size_t(b)] = cfg->recoverable[b] ? 1 : 0;
+
+  hipError_t e = hipSuccess;
+  if (!items.empty())
+    e = hipMemcpyAsync(c->d_items, items.data(), items.size() * sizeof(Item),
+                       hipMemcpyHostToDevice, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->d_unit_item_off, unit_item_off.data(),
+                       unit_item_off.size() * sizeof(int64_t), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess && S > 0)
+    e = hipMemcpyAsync(c->d_seg_dtype, c->seg_dtype.data(), size_t(S) * sizeof(int32_t),
+                       hipMemcpyHostToDevice, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->d_rec, rec.data(), rec.size(), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_A, 0, size_t(U) * sizeof(double), st);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->d_Q, 0, size_t(U) * size_t(c->window) * sizeof(double), st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_lock, 0, size_t(U) * sizeof(int32_t), st);
+  if (e == hipSuccess && S > 0)
+    e = hipMemsetAsync(c->d_seg_base, 0, size_t(S) * sizeof(void*), st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return bail(GNMR_E_HIP, std::string("init upload: ") + hipGetErrorString(e));
+
+  if (segs->seg_ptr != nullptr) {
+    gnmr_status r = bind_ptrs(c, segs->seg_ptr, st);
+    if (r == GNMR_OK && hipStreamSynchronize(st) != hipSuccess)
+      r = fail(GNMR_E_HIP, "init pointer upload failed");
+    if (r != GNMR_OK) {
+      std::string m = g_last_error;
+      return bail(r, m);
+    }
+  }
+  *out = c;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_destroy(gnmr_ctx* ctx) {
+  if (ctx == nullptr) return GNMR_OK;
+  DeviceGuard g(ctx->device);
+  release(ctx);
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_step(gnmr_ctx* ctx, double alpha_t, double beta_t, const void* const* seg_ptr,
+                      void* stream) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  gnmr_status r = check_thresholds(alpha_t, beta_t);
+  if (r != GNMR_OK) return r;
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  r = bind_ptrs(ctx, seg_ptr, st);
+  if (r != GNMR_OK) return r;
+  r = record(ctx, 0, st);
+  if (r != GNMR_OK) return r;
+  GNMR_HIP(gnmr::launch_sumsq(ctx->d_items, ctx->num_items, ctx->d_seg_base, ctx->d_seg_dtype,
+                              ctx->d_partial, st));
+  r = record(ctx, 1, st);
+  if (r != GNMR_OK) return r;
+  return update_and_select(ctx, nullptr, alpha_t, beta_t, st);
+}
+
+gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm, double alpha_t,
+                                 double beta_t, void* stream) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (d_norm == nullptr) return fail(GNMR_E_INVALID, "d_norm is NULL");
+  gnmr_status r = check_thresholds(alpha_t, beta_t);
+  if (r != GNMR_OK) return r;
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  r = record(ctx, 0, st);
+  if (r == GNMR_OK) r = record(ctx, 1, st);
+  if (r != GNMR_OK) return r;
+  return update_and_select(ctx, d_norm, alpha_t, beta_t, st);
+}
+
+gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr, double* d_sumsq,
+                       void* stream) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (d_sumsq == nullptr) return fail(GNMR_E_INVALID, "d_sumsq is NULL");
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  gnmr_status r = bind_ptrs(ctx, seg_ptr, st);
+  if (r != GNMR_OK) return r;
+  GNMR_HIP(gnmr::launch_sumsq(ctx->d_items, ctx->num_items, ctx->d_seg_base, ctx->d_seg_dtype,
+                              ctx->d_partial, st));
+  GNMR_HIP(gnmr::launch_unit_sumsq(ctx->d_unit_item_off, ctx->d_partial, ctx->U, d_sumsq, st));
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_query(gnmr_ctx* ctx, uint8_t* mask, int32_t* lock, double* norm, double* gnmr,
+                       double* dgnmr, double* risk, gnmr_stats* stats, void* stream) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (ctx->t == 0) return fail(GNMR_E_STATE, "no step has been taken yet");
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t U = size_t(ctx->U);
+  auto d2h = [&](void* dst, const void* src, size_t bytes) -> hipError_t {
+    if (dst == nullptr) return hipSuccess;
+    return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, st);
+  };
+  GNMR_HIP(d2h(mask, ctx->d_mask, U));
+  GNMR_HIP(d2h(lock, ctx->d_lock, U * sizeof(int32_t)));
+  GNMR_HIP(d2h(norm, ctx->d_norm, U * sizeof(double)));
+  GNMR_HIP(d2h(gnmr, ctx->d_gnmr, U * sizeof(double)));
+  GNMR_HIP(d2h(dgnmr, ctx->d_dgnmr, U * sizeof(double)));
+  GNMR_HIP(d2h(risk, ctx->d_risk, U * sizeof(double)));
+  GNMR_HIP(d2h(stats, ctx->d_stats, sizeof(gnmr_stats)));
+  GNMR_HIP(hipStreamSynchronize(st));
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_device_outputs(gnmr_ctx* ctx, const uint8_t** mask, const int32_t** lock,
+                                const double** norm, const double** gnmr, const double** dgnmr,
+                                const double** risk, const gnmr_stats** stats) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (mask) *mask = ctx->d_mask;
+  if (lock) *lock = ctx->d_lock;
+  if (norm) *norm = ctx->d_norm;
+  if (gnmr) *gnmr = ctx->d_gnmr;
+  if (dgnmr) *dgnmr = ctx->d_dgnmr;
+  if (risk) *risk = ctx->d_risk;
+  if (stats) *stats = ctx->d_stats;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_state_size(const gnmr_ctx* ctx, size_t* bytes) {
+  if (ctx == nullptr || bytes == nullptr) return fail(GNMR_E_INVALID, "NULL argument");
+  const size_t U = size_t(ctx->U);
+  *bytes = sizeof(StateHeader) + U * sizeof(double) * (1 + size_t(ctx->window)) +
+           U * sizeof(int32_t);
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream) {
+  size_t need = 0;
+  gnmr_status r = gnmr_state_size(ctx, &need);
+  if (r != GNMR_OK) return r;
+  if (buf == nullptr || bytes < need) return fail(GNMR_E_INVALID, "state buffer too small");
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  StateHeader h{kStateMagic, kStateVersion, ctx->U, ctx->window, ctx->t,
+                ctx->max_o, ctx->lock_len, ctx->eps};
+  char* p = static_cast<char*>(buf);
+  memcpy(p, &h, sizeof h);
+  p += sizeof h;
+  const size_t U = size_t(ctx->U);
+  GNMR_HIP(hipMemcpyAsync(p, ctx->d_A, U * sizeof(double), hipMemcpyDeviceToHost, st));
+  p += U * sizeof(double);
+  GNMR_HIP(hipMemcpyAsync(p, ctx->d_Q, U * size_t(ctx->window) * sizeof(double),
+                          hipMemcpyDeviceToHost, st));
+  p += U * size_t(ctx->window) * sizeof(double);
+  GNMR_HIP(hipMemcpyAsync(p, ctx->d_lock, U * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  GNMR_HIP(hipStreamSynchronize(st));
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* stream) {
+  size_t need = 0;
+  gnmr_status r = gnmr_state_size(ctx, &need);
+  if (r != GNMR_OK) return r;
+  if (buf == nullptr || bytes != need) return fail(GNMR_E_INVALID, "state blob size mismatch");
+  StateHeader h;
+  memcpy(&h, buf, sizeof h);
+  if (h.magic != kStateMagic || h.version != kStateVersion)
+    return fail(GNMR_E_INVALID, "not a GNMR state blob of this version");
+  if (h.num_units != ctx->U || h.window != ctx->window)
+    return fail(GNMR_E_INVALID, "state blob is for a different num_units or window");
+  if (h.t < 0) return fail(GNMR_E_INVALID, "state blob has a negative step counter");
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const char* p = static_cast<const char*>(buf) + sizeof h;
+  const size_t U = size_t(ctx->U);
+  GNMR_HIP(hipMemcpyAsync(ctx->d_A, p, U * sizeof(double), hipMemcpyHostToDevice, st));
+  p += U * sizeof(double);
+  GNMR_HIP(hipMemcpyAsync(ctx->d_Q, p, U * size_t(ctx->window) * sizeof(double),
+                          hipMemcpyHostToDevice, st));
+  p += U * size_t(ctx->window) * sizeof(double);
+  GNMR_HIP(hipMemcpyAsync(ctx->d_lock, p, U * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  GNMR_HIP(hipStreamSynchronize(st));
+  ctx->t = h.t;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_set_profiling(gnmr_ctx* ctx, int enable) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  ctx->prof = enable != 0;
+  ctx->prof_steps = 0;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_profile_read(gnmr_ctx* ctx, double* ms_sumsq, double* ms_update,
+                              double* ms_select, int64_t* steps) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  DeviceGuard g(ctx->device);
+  double acc[3] = {0, 0, 0};
+  for (int64_t i = 0; i < ctx->prof_steps; ++i) {
+    auto& ev = ctx->prof_ev[size_t(i)];
+    GNMR_HIP(hipEventSynchronize(ev[3]));
+    for (int k = 0; k < 3; ++k) {
+      float ms = 0.f;
+      GNMR_HIP(hipEventElapsedTime(&ms, ev[k], ev[k + 1]));
+      acc[k] += ms;
+    }
+  }
+  if (ms_sumsq) *ms_sumsq = acc[0];
+  if (ms_update) *ms_update = acc[1];
+  if (ms_select) *ms_select = acc[2];
+  if (steps) *steps = ctx->prof_steps;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_info(const gnmr_ctx* ctx, int64_t* num_items, int64_t* item_bytes,
+                      int64_t* bytes_per_step, int32_t* launches_per_step) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (num_items) *num_items = ctx->num_items;
+  if (item_bytes) *item_bytes = gnmr::kItemBytes;
+  if (bytes_per_step) *bytes_per_step = ctx->bytes_per_step;
+  if (launches_per_step) *launches_per_step = ctx->num_items > 0 ? 3 : 2;
+  return GNMR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,69 @@
+"""The C-ABI library loads on a host without a GPU, exports every entry point
+that include/gnmr.h declares, and rejects bad configurations before touching
+the device.  CPU only."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_entry_points():
+    text = open(os.path.join(ROOT, "include", "gnmr.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gnmr_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_entry_points()
+    for n in ("gnmr_init", "gnmr_step", "gnmr_query", "gnmr_destroy", "gnmr_step_from_norms",
+              "gnmr_get_state", "gnmr_set_state", "gnmr_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2606_00539_amd import binding as B
+
+    lib = B.load_library()
+    missing = [n for n in declared_entry_points() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(B.EXPORTED) == set(declared_entry_points())
+
+
+def test_struct_layouts_match_header():
+    import ctypes
+
+    from paper_2606_00539_amd import binding as B
+
+    assert ctypes.sizeof(B.gnmr_config) == 32
+    assert ctypes.sizeof(B.gnmr_segments) == 40
+    assert ctypes.sizeof(B.gnmr_stats) == 40
+
+
+@pytest.mark.parametrize("bad", [
+    dict(num_units=0), dict(window=0), dict(max_o=-1), dict(lock_len=-2), dict(eps=-1.0),
+    dict(eps=float("nan")), dict(unit_seg_off=[0, 2, 1]), dict(unit_seg_off=[1, 1, 1]),
+    dict(seg_numel=[-1]), dict(seg_dtype=[7]),
+])
+def test_init_rejects_bad_configuration(bad):
+    from paper_2606_00539_amd import GnmrError, gnmr_init
+    from paper_2606_00539_amd import binding as B
+
+    args = dict(num_units=2, window=5, max_o=1, lock_len=1, eps=0.0,
+                unit_seg_off=[0, 1, 1], seg_numel=[10], seg_dtype=[B.GNMR_BF16])
+    args.update(bad)
+    if "unit_seg_off" in bad and bad["unit_seg_off"][-1] != 1:
+        args["num_units"] = len(bad["unit_seg_off"]) - 1
+    with pytest.raises(GnmrError) as e:
+        gnmr_init(**args)
+    assert e.value.status == B.GNMR_E_INVALID
+    assert B.gnmr_last_error() != ""
+
+
+def test_two_stage_schedule():
+    from paper_2606_00539_amd import two_stage_alpha
+
+    assert [two_stage_alpha(t, 256) for t in (1, 7, 8, 256)] == [1.5, 1.5, 1.1, 1.1]
+    assert two_stage_alpha(1, 16) == 1.5 and two_stage_alpha(2, 16) == 1.1

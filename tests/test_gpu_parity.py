@@ -1,0 +1,283 @@
+"""Parity of the HIP controller pass (through the C ABI) with the CPU oracle.
+
+Bars: masks, locks and counters bit-exact; norms, GNMR, Delta-GNMR and R
+within 1e-5 relative (fp32 accumulation of squares against float64).  Inputs
+are seeded and synthetic; decisions are kept at least 1e-4 away from every
+threshold (see tests/streams.py) so that bit-exact masks are well defined.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import streams as S
+from gpu_util import assert_step_matches, controller_for, device_buffer, require_gpu
+from oracle import Controller as Oracle
+from oracle import sumsq as oracle_sumsq
+from synth import layout as L
+from synth import recipe as R
+from synth import values as V
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def gen():
+    require_gpu()
+    from synth.gpu import Generator
+
+    return Generator()
+
+
+def test_tiny_end_to_end(gen):
+    torch = require_gpu()
+    w = R.get("tiny")
+    say("tiny end-to-end:", w.description)
+    nudge, _, ref, alphas, betas = S.guarded_stream(
+        w, lambda t, s32, units: S.host_norms(w, t, s32, units))
+    lay = L.for_workload(w)
+    buf, base, ptrs = device_buffer(torch, lay)
+    with controller_for(lay, w, ptrs) as ctl:
+        assert ctl.info()["launches_per_step"] == 3
+        for t in range(1, w.steps + 1):
+            gen.fill(lay, base, w.seed, t, w.scale32(t, nudge[t - 1]))
+            ctl.step(alphas[t - 1], betas[t - 1])
+            assert_step_matches(ctl.query(), ref[t - 1], what=f"t={t}")
+    # the generator is bit-identical to the host twin (last step, two units)
+    for b in (0, 27):
+        s = int(lay.seg_byte_off[b])
+        n = int(lay.seg_numel[b])
+        dev = buf[s:s + 4 * n].cpu().numpy().view(np.float32)
+        host = V.unit_values(w.seed, w.steps, b, float(w.scale32(w.steps, nudge[-1])[b]),
+                             V.DTYPE_F32, 0, n)
+        assert np.array_equal(dev, host)
+
+
+def ragged_layout(rng, misaligned: bool):
+    sizes = [0, 1, 7, 8, 9, 4095, 32767, 32768, 32769, 65536 * 3 + 5, 1_000_003, 123_457, 2]
+    dtypes = [int(rng.integers(0, 2)) for _ in sizes]
+    pieces = []
+    for n in sizes:
+        if n > 20 and rng.random() < 0.6:
+            cuts = sorted(rng.choice(np.arange(1, n), size=int(rng.integers(1, 4)), replace=False))
+            p = np.diff([0, *cuts, n]).tolist()
+            p.insert(int(rng.integers(0, len(p) + 1)), 0)     # an empty segment
+            pieces.append(p)
+        elif n == 0:
+            pieces.append([])                                # a unit with no segment
+        else:
+            pieces.append([n])
+    nseg = sum(len(p) for p in pieces)
+    shift = None
+    if misaligned:
+        shift = []
+        for b, p in enumerate(pieces):
+            esz = V.DTYPE_SIZE[dtypes[b]]
+            shift += [int(rng.integers(0, 16 // esz)) * esz for _ in p]
+        assert len(shift) == nseg
+    return L.build(sizes, dtypes, pieces=pieces, shift=shift), sizes, dtypes, pieces
+
+
+@pytest.mark.parametrize("misaligned", [False, True])
+def test_sumsq_ragged_layouts(gen, misaligned):
+    torch = require_gpu()
+    rng = np.random.default_rng(7 if misaligned else 8)
+    lay, sizes, dtypes, pieces = ragged_layout(rng, misaligned)
+    say("ragged sumsq: misaligned", misaligned, "segments", lay.num_segments)
+    buf, base, ptrs = device_buffer(torch, lay)
+    scale = (10.0 ** rng.uniform(-4, -2, size=len(sizes))).astype(np.float32)
+    gen.fill(lay, base, 5, 3, scale)
+    out = torch.zeros(len(sizes), dtype=torch.float64, device="cuda")
+    out2 = torch.zeros_like(out)
+    with controller_for(lay, ptrs=ptrs, window=5, max_o=2, lock_len=1, eps=0.0) as ctl:
+        ctl.sumsq(out)
+        ctl.sumsq(out2)
+        torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    assert np.array_equal(got, out2.cpu().numpy())                 # deterministic
+    for b, n in enumerate(sizes):
+        segs, start = [], 0
+        for m in pieces[b]:
+            segs.append((V.unit_values(5, 3, b, float(scale[b]), dtypes[b], start, m), dtypes[b]))
+            start += m
+        ref = oracle_sumsq(segs)
+        if n == 0:
+            assert got[b] == 0.0
+        else:
+            assert abs(got[b] - ref) <= 5e-6 * ref, (b, n, got[b], ref)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama2-7b", "llama2-13b", "moe", "fine128", "fine32"])
+def test_logic_from_norms(name):
+    """Alg. 1 + Alg. 2 on norm streams shaped like each workload: with identical
+    float64 norms both sides do identical IEEE arithmetic."""
+    torch = require_gpu()
+    w = R.get(name)
+    norms = R.surrogate_norms(w)
+    say("norm-level parity:", name, "units", w.num_units, "steps", w.steps)
+    from paper_2606_00539_amd import Controller
+
+    ora = Oracle(w.num_units, window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=w.eps)
+    dn = torch.empty(w.num_units, dtype=torch.float64, device="cuda")
+    with Controller(w.num_units, w.window, w.max_o, w.lock_len, w.eps, np.zeros(w.num_units + 1),
+                    [], []) as ctl:
+        for t in range(1, w.steps + 1):
+            dn.copy_(torch.from_numpy(norms[t - 1]))
+            ctl.step_from_norms(dn, w.alpha(t), w.beta(t))
+            ref = ora.step(norms[t - 1], w.alpha(t), w.beta(t))
+            assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{name} t={t}")
+
+
+def upload_units(torch, arrays):
+    """Place host arrays (float32) as one fp32 segment each; returns the layout
+    and the buffer."""
+    lay = L.build([a.size for a in arrays], [V.DTYPE_F32] * len(arrays))
+    buf, base, ptrs = device_buffer(torch, lay)
+    for a, off in zip(arrays, lay.seg_byte_off):
+        buf[int(off):int(off) + 4 * a.size].copy_(torch.from_numpy(a.view(np.uint8)))
+    return lay, buf, ptrs
+
+
+def test_constant_magnitude_is_exactly_one():
+    torch = require_gpu()
+    rng = np.random.default_rng(0)
+    mags = [2.0 ** -10, 2.0 ** -7]
+    lay = None
+    with torch.no_grad():
+        arrays = [np.where(rng.random(40_000 + 17 * i) < 0.5, -m, m).astype(np.float32)
+                  for i, m in enumerate(mags)]
+        lay, buf, ptrs = upload_units(torch, arrays)
+        with controller_for(lay, ptrs=ptrs, window=5, max_o=1, lock_len=2, eps=0.0) as ctl:
+            for t in range(1, 21):
+                for a, off in zip(arrays, lay.seg_byte_off):     # fresh signs, same magnitude
+                    rng.shuffle(a)
+                    buf[int(off):int(off) + 4 * a.size].copy_(torch.from_numpy(a.view(np.uint8)))
+                ctl.step(1.1, 1.5)
+                out = ctl.query()
+                assert np.all(out["gnmr"] == 1.0) and np.all(out["dgnmr"] == 1.0)
+                assert out["mask"].sum() == 0
+
+
+def test_spike_closed_form_on_gpu():
+    torch = require_gpu()
+    c, N, t0, k, delta = 2.0 ** -10, 1 << 16, 9, 20, 5
+    base = np.full(N, c, dtype=np.float32)
+    base[1::2] *= -1
+    lay, buf, ptrs = upload_units(torch, [base.copy(), base.copy()])
+    off = int(lay.seg_byte_off[0])
+    with controller_for(lay, ptrs=ptrs, window=delta, max_o=1, lock_len=3, eps=0.0) as ctl:
+        hist = []
+        for t in range(1, t0 + 4):
+            g = base * np.float32(k if t == t0 else 1)
+            buf[off:off + 4 * N].copy_(torch.from_numpy(g.view(np.uint8)))
+            ctl.step(1.1, 1.5)
+            out = ctl.query()
+            hist.append(out)
+        assert hist[t0 - 1]["gnmr"][0] == k and hist[t0 - 1]["dgnmr"][0] == k
+        assert hist[t0 - 1]["mask"].tolist() == [1, 0]
+        assert abs(hist[t0]["gnmr"][0] - t0 / (t0 - 1 + k)) < 1e-15
+        assert abs(hist[t0]["dgnmr"][0] - delta * t0 / ((t0 - 1 + k) * (delta - 1 + k))) < 1e-15
+        assert [h["mask"][0] for h in hist[t0 - 1:]] == [1, 1, 1, 1]   # lock 3 holds
+
+
+def test_state_roundtrip_is_bitwise():
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller
+
+    w = R.get("moe")
+    norms = R.surrogate_norms(w)
+    dn = torch.empty(w.num_units, dtype=torch.float64, device="cuda")
+    mk = lambda: Controller(w.num_units, w.window, w.max_o, w.lock_len, w.eps,
+                            np.zeros(w.num_units + 1), [], [])
+    a, b = mk(), mk()
+    for t in range(1, 13):
+        dn.copy_(torch.from_numpy(norms[t - 1]))
+        a.step_from_norms(dn, w.alpha(t), w.beta(t))
+    b.set_state(a.get_state())
+    for t in range(13, w.steps + 1):
+        dn.copy_(torch.from_numpy(norms[t - 1]))
+        a.step_from_norms(dn, w.alpha(t), w.beta(t))
+        b.step_from_norms(dn, w.alpha(t), w.beta(t))
+        qa, qb = a.query(), b.query()
+        for f in ("mask", "lock", "norm", "gnmr", "dgnmr", "risk"):
+            assert np.array_equal(qa[f], qb[f])
+        assert qa["stats"] == qb["stats"]
+    a.close()
+    b.close()
+
+
+@pytest.mark.parametrize("case", ["maxo0", "alpha_below_one", "nonfinite", "not_recoverable",
+                                  "window1_lock0"])
+def test_edge_cases(case):
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller
+
+    rng = np.random.default_rng(3)
+    U, T = 300, 24
+    norms = np.exp(rng.normal(scale=0.3, size=(T, U)))
+    norms[10, 5] *= 30
+    window, max_o, lock_len, alpha = 5, 8, 3, 1.1
+    rec = None
+    if case == "maxo0":
+        max_o = 0
+    elif case == "alpha_below_one":
+        alpha = 0.4
+    elif case == "nonfinite":
+        norms[12, 7] = np.nan
+        norms[12, 9] = np.inf
+        norms[13, 7] = np.inf
+    elif case == "not_recoverable":
+        rec = (rng.random(U) < 0.5).astype(np.uint8)
+        rec[5] = 0
+    elif case == "window1_lock0":
+        window, lock_len = 1, 0
+    ora = Oracle(U, window=window, max_o=max_o, lock_len=lock_len, eps=1e-12, recoverable=rec)
+    dn = torch.empty(U, dtype=torch.float64, device="cuda")
+    with Controller(U, window, max_o, lock_len, 1e-12, np.zeros(U + 1), [], [],
+                    recoverable=rec) as ctl:
+        for t in range(1, T + 1):
+            dn.copy_(torch.from_numpy(norms[t - 1]))
+            ctl.step_from_norms(dn, alpha, 1.5)
+            ref = ora.step(norms[t - 1], alpha, 1.5)
+            assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} t={t}")
+
+
+def test_abi_errors_leave_state_unchanged():
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller, GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    U = 4
+    dn = torch.ones(U, dtype=torch.float64, device="cuda")
+    with Controller(U, 5, 1, 1, 0.0, np.zeros(U + 1), [], []) as ctl:
+        with pytest.raises(GnmrError) as e:
+            ctl.query()
+        assert e.value.status == B.GNMR_E_STATE
+        ctl.step_from_norms(dn, 1.1, 1.5)
+        blob = ctl.get_state()
+        for a, b_ in ((0.0, 1.5), (1.1, -1.0), (float("inf"), 1.5), (1.1, float("nan"))):
+            with pytest.raises(GnmrError) as e:
+                ctl.step_from_norms(dn, a, b_)
+            assert e.value.status == B.GNMR_E_INVALID
+        assert ctl.get_state() == blob
+        assert ctl.query()["stats"]["t"] == 1
+        with pytest.raises(GnmrError):
+            ctl.set_state(blob[:-1])
+    # a misaligned segment pointer is rejected
+    buf = torch.zeros(1024, dtype=torch.uint8, device="cuda")
+    with pytest.raises(GnmrError) as e:
+        Controller(1, 5, 1, 1, 0.0, [0, 1], [10], [B.GNMR_F32], [buf.data_ptr() + 2])
+    assert e.value.status == B.GNMR_E_INVALID
+    # no pointers bound and none passed
+    with Controller(1, 5, 1, 1, 0.0, [0, 1], [10], [B.GNMR_F32]) as ctl:
+        with pytest.raises(GnmrError) as e:
+            ctl.step(1.1, 1.5)
+        assert e.value.status == B.GNMR_E_INVALID
+        ctl.step(1.1, 1.5, seg_ptr=[buf.data_ptr()])
+        ctl.step(1.1, 1.5)                                   # reuses bound pointers
+        assert ctl.query()["stats"]["t"] == 2
