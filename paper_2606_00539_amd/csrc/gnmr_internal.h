@@ -13,6 +13,8 @@ namespace gnmr {
 constexpr int kK1Block = 256;
 constexpr int kK1Unroll = 16;
 constexpr int64_t kItemBytes = int64_t(kK1Block) * kK1Unroll * 16;
+// MI355X: 256 compute units in 8 XCDs, each XCD with its own L2.
+constexpr uint32_t kNumXcd = 8;
 
 // One work item: elements [e0, e0 + count) of segment `seg`.  Items are
 // ordered by unit, so the items of unit b are [unit_item_off[b],
@@ -25,7 +27,14 @@ struct Item {
 static_assert(sizeof(Item) == 16, "Item layout");
 
 // Per-unit flag bits written by K2 and read by K3.
-enum : uint8_t { kFlagTrigG = 1, kFlagTrigD = 2, kFlagNonFinite = 4 };
+enum : uint8_t {
+  kFlagTrigG = 1,      // GNMR / alpha > 1
+  kFlagTrigD = 2,      // Delta-GNMR / beta > 1
+  kFlagNonFinite = 4,  // non-finite norm
+  kFlagTrigR = 8,      // R > 1
+  kFlagRec = 16,       // recoverable
+  kFlagCand = 32       // member of the candidate pool C_t
+};
 
 struct UpdateArgs {
   int32_t num_units;
@@ -43,6 +52,9 @@ struct UpdateArgs {
   double* gnmr;
   double* dgnmr;
   double* risk;
+  const uint8_t* rec;            // [U]
+  const int32_t* lock;           // [U], Lock after step t-1
+  uint64_t* keys;                // [U], candidate key or 0
   uint8_t* flags;
 };
 
@@ -51,9 +63,8 @@ struct SelectArgs {
   int32_t max_o;
   int32_t lock_len;
   int64_t t;
-  const double* risk;
   const uint8_t* flags;
-  const uint8_t* rec;
+  const uint64_t* keys;
   int32_t* lock;       // in: Lock after step t-1; out: after step t
   uint8_t* mask;
   gnmr_stats* stats;
@@ -62,8 +73,8 @@ struct SelectArgs {
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,
                         const int32_t* seg_dtype, float* partial, hipStream_t s);
 hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,
-                             int32_t num_units, double* out, hipStream_t s);
-hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
-hipError_t launch_select(const SelectArgs& a, uint64_t* keys, hipStream_t s);
+                             int64_t num_items, int32_t num_units, double* out, hipStream_t s);
+hipError_t launch_update(const UpdateArgs& a, int64_t num_items, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 
 }  // namespace gnmr

@@ -74,6 +74,12 @@ typedef __attribute__((address_space(1))) const u32x4 g_vec;
 typedef __attribute__((address_space(1))) const uint16_t g_u16;
 typedef __attribute__((address_space(1))) const float g_f32;
 
+// Streaming loads: every gradient byte is read exactly once, so the loads
+// carry the non-temporal hint and do not displace cache lines worth keeping.
+__device__ __forceinline__ u32x4 stream_load(const g_vec* p) {
+  return __builtin_nontemporal_load(p);
+}
+
 // The 16-byte-aligned body of one item: lane i reads vectors i, i + 256, ...
 // All 16 loads are issued before the first is consumed.  In a ragged item
 // lanes past the end re-read the last vector (always in bounds) and add zero.
@@ -83,12 +89,12 @@ __device__ __forceinline__ void body_sumsq(const g_vec* body, int nvec, int tid,
   u32x4 v[kK1Unroll];
   if (nvec == kK1Block * kK1Unroll) {
 #pragma unroll
-    for (int k = 0; k < kK1Unroll; ++k) v[k] = body[tid + k * kK1Block];
+    for (int k = 0; k < kK1Unroll; ++k) v[k] = stream_load(body + tid + k * kK1Block);
   } else if (nvec > 0) {
 #pragma unroll
     for (int k = 0; k < kK1Unroll; ++k) {
       const int i = tid + k * kK1Block;
-      v[k] = body[i < nvec ? i : nvec - 1];
+      v[k] = stream_load(body + (i < nvec ? i : nvec - 1));
     }
 #pragma unroll
     for (int k = 0; k < kK1Unroll; ++k)
@@ -100,11 +106,23 @@ __device__ __forceinline__ void body_sumsq(const g_vec* body, int nvec, int tid,
   for (int k = 0; k < kK1Unroll; ++k) acc_vec<DT>(v[k], a0, a1, a2, a3);
 }
 
+// Workgroups are dispatched to the eight XCDs round-robin (workgroup w runs
+// on XCD w % 8).  Give each XCD one contiguous eighth of the item list, so
+// that each XCD's L2 and address translation see a single sequential stream.
+// A bijection of [0, num_items) for any num_items.
+__device__ __forceinline__ uint32_t xcd_item(uint32_t w, uint32_t num_items) {
+  const uint32_t x = w % kNumXcd, j = w / kNumXcd;
+  const uint32_t q = num_items / kNumXcd, r = num_items % kNumXcd;
+  return x * q + (x < r ? x : r) + j;
+}
+
 __global__ __launch_bounds__(kK1Block) void k1_sumsq(const Item* __restrict__ items,
+                                                     uint32_t num_items,
                                                      const char* const* __restrict__ seg_base,
                                                      const int32_t* __restrict__ seg_dtype,
                                                      float* __restrict__ partial) {
-  const Item it = items[blockIdx.x];
+  const uint32_t item = xcd_item(blockIdx.x, num_items);
+  const Item it = items[item];
   const int dt = seg_dtype[it.seg];
   const uintptr_t esz = dt == GNMR_BF16 ? 2 : 4;
   const uintptr_t b0 = reinterpret_cast<uintptr_t>(seg_base[it.seg]) + uintptr_t(it.e0) * esz;
@@ -143,38 +161,69 @@ __global__ __launch_bounds__(kK1Block) void k1_sumsq(const Item* __restrict__ it
   __shared__ float red[kK1Block / 64];
   if ((tid & 63) == 0) red[tid >> 6] = s;
   __syncthreads();
-  if (tid == 0) partial[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+  if (tid == 0) partial[item] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-// Fixed-order float64 sum of unit b's item partials by one wavefront.
+// Fixed-order float64 sum of unit b's item partials by L lanes (lane < L):
+// each lane keeps four running sums over a stride-L walk, then the lanes are
+// combined by a fixed butterfly (and, for L = 256, a fixed cross-wave order).
+template <int L>
 __device__ __forceinline__ double unit_ss(const int64_t* __restrict__ off,
-                                          const float* __restrict__ partial, int b, int lane) {
-  double s = 0.0;
+                                          const float* __restrict__ partial, int b, int lane,
+                                          double* red) {
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
   const int64_t hi = off[b + 1];
-  for (int64_t i = off[b] + lane; i < hi; i += 64) s += double(partial[i]);
-  return wave_sum(s);
+  int64_t i = off[b] + lane;
+  for (; i + 3 * L < hi; i += 4 * L) {
+    const float a = partial[i], c = partial[i + L], d = partial[i + 2 * L], e = partial[i + 3 * L];
+    s0 += double(a);
+    s1 += double(c);
+    s2 += double(d);
+    s3 += double(e);
+  }
+  for (; i < hi; i += L) s0 += double(partial[i]);
+  double s = wave_sum((s0 + s1) + (s2 + s3));
+  if constexpr (L == 64) {
+    return s;
+  } else {
+    static_assert(L == 256, "64 or 256 lanes per unit");
+    if ((lane & 63) == 0) red[lane >> 6] = s;
+    __syncthreads();
+    return ((red[0] + red[1]) + red[2]) + red[3];
+  }
 }
 
+template <int L>
 __global__ __launch_bounds__(256) void k_unit_sumsq(const int64_t* __restrict__ off,
                                                     const float* __restrict__ partial,
                                                     int num_units, double* __restrict__ out) {
-  const int lane = threadIdx.x & 63;
-  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (b >= num_units) return;
-  const double s = unit_ss(off, partial, b, lane);
+  __shared__ double red[4];
+  const int lane = threadIdx.x % L;
+  const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
+  if (b >= num_units) return;  // uniform per workgroup when L = 256
+  const double s = unit_ss<L>(off, partial, b, lane, red);
   if (lane == 0) out[b] = s;
 }
 
-// K2: one wavefront per unit.
+// Order-preserving key of a candidate: R >= 0 (or +inf), so its IEEE bits
+// are monotone in R; +1 keeps 0 free for "not a candidate".
+__device__ __forceinline__ uint64_t cand_key(double R) {
+  return uint64_t(__double_as_longlong(R)) + 1;
+}
+
+// K2: L lanes per unit sum its partials; lane 0 then runs Alg. 1, the risk of
+// Alg. 2, and marks the unit's membership of the candidate pool C_t.
+template <int L>
 __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (b >= a.num_units) return;
+  __shared__ double red[4];
+  const int lane = threadIdx.x % L;
+  const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
+  if (b >= a.num_units) return;  // uniform per workgroup when L = 256
   double n;
   if (a.ext_norm != nullptr) {
     n = a.ext_norm[b];
   } else {
-    n = sqrt(unit_ss(a.unit_item_off, a.partial, b, lane));
+    n = sqrt(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
   }
   if (lane != 0) return;
 
@@ -201,31 +250,43 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   a.Q[int64_t(a.slot) * U + b] = finite ? G : 1.0;
   if (!finite) G = D = INFINITY;
 
-  // Alg. 2: R = max(GNMR / alpha, Delta-GNMR / beta).
+  // Alg. 2: R = max(GNMR / alpha, Delta-GNMR / beta); the pool C_t holds the
+  // recoverable units with R > 1 or a lock left from the previous step.
   const double gt = G / a.alpha;
   const double dt = D / a.beta;
   const double R = gt > dt ? gt : dt;
+  const bool rec = a.rec[b] != 0;
+  const bool trig = R > 1.0;
+  const bool cand = rec && (trig || a.lock[b] > 0);
   a.norm[b] = n;
   a.gnmr[b] = G;
   a.dgnmr[b] = D;
   a.risk[b] = R;
+  a.keys[b] = cand ? cand_key(R) : 0;
   a.flags[b] = uint8_t((gt > 1.0 ? kFlagTrigG : 0) | (dt > 1.0 ? kFlagTrigD : 0) |
-                       (finite ? 0 : kFlagNonFinite));
+                       (finite ? 0 : kFlagNonFinite) | (trig ? kFlagTrigR : 0) |
+                       (rec ? kFlagRec : 0) | (cand ? kFlagCand : 0));
 }
 
 constexpr int kK3Block = 1024;
 
-// Order-preserving key of a candidate: R >= 0 (or +inf), so its IEEE bits
-// are monotone in R; +1 keeps 0 free for "not a candidate".
-__device__ __forceinline__ uint64_t cand_key(double R) {
-  return uint64_t(__double_as_longlong(R)) + 1;
+// Lock update of Alg. 2 for one unit given its selection.
+__device__ __forceinline__ void apply_selection(const SelectArgs& a, int b, bool sel, uint8_t f) {
+  int32_t L = 0;
+  if (sel) {
+    const int32_t prev = a.lock[b];
+    L = (f & kFlagTrigR) ? a.lock_len : (prev > 0 ? prev - 1 : 0);
+  }
+  a.lock[b] = L;
+  a.mask[b] = sel ? 1 : 0;
 }
 
-// K3: a single workgroup.  Top_maxO is a radix select over the 64-bit keys
-// (8 passes of 8 bits, most significant first) for the maxO-th largest key
-// T; then every candidate with key > T is active, and the first `need`
-// candidates with key == T in index order.
-__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a, uint64_t* __restrict__ keys) {
+// K3: a single workgroup.  When |C_t| <= maxO every candidate is active.
+// Otherwise Top_maxO is a radix select over the 64-bit keys (8 passes of 8
+// bits, most significant first) for the maxO-th largest key T; every
+// candidate with key > T is active, and the first `need` candidates with
+// key == T in index order.
+__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
   __shared__ int cnt[6];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t scan[kK3Block];
@@ -237,35 +298,35 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a, uint64_t* __
 
   int c_cand = 0, c_tg = 0, c_td = 0, c_tr = 0, c_nf = 0;
   for (int b = tid; b < U; b += kK3Block) {
-    const double R = a.risk[b];
     const uint8_t f = a.flags[b];
-    const bool rec = a.rec[b] != 0;
-    const bool trig = R > 1.0;
-    const bool cand = rec && (trig || a.lock[b] > 0);
-    keys[b] = cand ? cand_key(R) : 0;
-    c_cand += cand;
-    if (rec) {
+    c_cand += (f & kFlagCand) != 0;
+    if (f & kFlagRec) {
       c_tg += (f & kFlagTrigG) != 0;
       c_td += (f & kFlagTrigD) != 0;
-      c_tr += trig;
+      c_tr += (f & kFlagTrigR) != 0;
     }
     c_nf += (f & kFlagNonFinite) != 0;
   }
-  atomicAdd(&cnt[0], c_cand);
-  atomicAdd(&cnt[1], c_tg);
-  atomicAdd(&cnt[2], c_td);
-  atomicAdd(&cnt[3], c_tr);
-  atomicAdd(&cnt[4], c_nf);
+  if (c_cand) atomicAdd(&cnt[0], c_cand);
+  if (c_tg) atomicAdd(&cnt[1], c_tg);
+  if (c_td) atomicAdd(&cnt[2], c_td);
+  if (c_tr) atomicAdd(&cnt[3], c_tr);
+  if (c_nf) atomicAdd(&cnt[4], c_nf);
   __syncthreads();
   const int n_cand = cnt[0];
 
-  uint64_t T;       // threshold key
-  int need = 0;     // how many keys equal to T to take, in index order
-  if (a.max_o == 0) {
-    T = ~uint64_t(0);
-  } else if (n_cand <= a.max_o) {
-    T = 0;          // every candidate (key >= 1)
+  int c_act = 0;
+  if (a.max_o == 0 || n_cand <= a.max_o) {
+    // A_t = C_t (or empty when maxO = 0): no ranking needed.
+    const bool take = a.max_o > 0;
+    for (int b = tid; b < U; b += kK3Block) {
+      const uint8_t f = a.flags[b];
+      const bool sel = take && (f & kFlagCand);
+      apply_selection(a, b, sel, f);
+      c_act += sel;
+    }
   } else {
+    const uint64_t* __restrict__ keys = a.keys;
     uint64_t prefix = 0, pmask = 0;
     int k = a.max_o;  // rank of T from the top, 1-based
     for (int shift = 56; shift >= 0; shift -= 8) {
@@ -292,45 +353,37 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a, uint64_t* __
       k = s_k;
       __syncthreads();
     }
-    T = prefix;
-    need = k;
-  }
+    const uint64_t T = prefix;  // >= 1: more than maxO keys are >= 1
+    const int need = k;         // keys equal to T to take, in index order
 
-  // Final pass over contiguous index ranges so that ties at T are ranked in
-  // index order: exclusive scan of per-thread tie counts.
-  const int per = (U + kK3Block - 1) / kK3Block;
-  const int lo = tid * per < U ? tid * per : U;
-  const int hi = lo + per < U ? lo + per : U;
-  uint32_t ties = 0;
-  if (need > 0)
+    // Contiguous index ranges per thread, so that ties at T are ranked in
+    // index order by an exclusive scan of per-thread tie counts.
+    const int per = (U + kK3Block - 1) / kK3Block;
+    const int lo = tid * per < U ? tid * per : U;
+    const int hi = lo + per < U ? lo + per : U;
+    uint32_t ties = 0;
     for (int b = lo; b < hi; ++b) ties += keys[b] == T;
-  scan[tid] = ties;
-  __syncthreads();
-  for (int d = 1; d < kK3Block; d <<= 1) {
-    const uint32_t v = tid >= d ? scan[tid - d] : 0;
+    scan[tid] = ties;
     __syncthreads();
-    scan[tid] += v;
-    __syncthreads();
-  }
-  uint32_t rank = scan[tid] - ties;  // ties before this thread's range
-  int c_act = 0;
-  for (int b = lo; b < hi; ++b) {
-    const uint64_t key = keys[b];
-    bool sel = key > T;
-    if (!sel && need > 0 && key == T) {
-      sel = rank < uint32_t(need);
-      ++rank;
+    for (int d = 1; d < kK3Block; d <<= 1) {
+      const uint32_t v = tid >= d ? scan[tid - d] : 0;
+      __syncthreads();
+      scan[tid] += v;
+      __syncthreads();
     }
-    int32_t L = 0;
-    if (sel) {
-      const int32_t prev = a.lock[b];
-      L = a.risk[b] > 1.0 ? a.lock_len : (prev > 0 ? prev - 1 : 0);
+    uint32_t rank = scan[tid] - ties;  // ties before this thread's range
+    for (int b = lo; b < hi; ++b) {
+      const uint64_t key = keys[b];
+      bool sel = key > T;
+      if (key == T) {
+        sel = rank < uint32_t(need);
+        ++rank;
+      }
+      apply_selection(a, b, sel, a.flags[b]);
+      c_act += sel;
     }
-    a.lock[b] = L;
-    a.mask[b] = sel ? 1 : 0;
-    c_act += sel;
   }
-  atomicAdd(&cnt[5], c_act);
+  if (c_act) atomicAdd(&cnt[5], c_act);
   __syncthreads();
   if (tid == 0) {
     gnmr_stats st;
@@ -352,25 +405,38 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a, uint64_t* __
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,
                         const int32_t* seg_dtype, float* partial, hipStream_t s) {
   if (num_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k1_sumsq, dim3(unsigned(num_items)), dim3(kK1Block), 0, s, items, seg_base,
-                     seg_dtype, partial);
+  hipLaunchKernelGGL(k1_sumsq, dim3(unsigned(num_items)), dim3(kK1Block), 0, s, items,
+                     uint32_t(num_items), seg_base, seg_dtype, partial);
   return hipGetLastError();
+}
+
+// Lanes per unit for the partial sums: a whole workgroup once a unit has
+// many items (long strided walks are latency bound), else one wavefront.
+static bool wide_units(const int64_t num_items, int32_t num_units) {
+  return num_items >= int64_t(num_units) * 512;
 }
 
 hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,
-                             int32_t num_units, double* out, hipStream_t s) {
-  hipLaunchKernelGGL(k_unit_sumsq, dim3(unsigned((num_units + 3) / 4)), dim3(256), 0, s,
-                     unit_item_off, partial, num_units, out);
+                             int64_t num_items, int32_t num_units, double* out, hipStream_t s) {
+  if (wide_units(num_items, num_units))
+    hipLaunchKernelGGL(k_unit_sumsq<256>, dim3(unsigned(num_units)), dim3(256), 0, s,
+                       unit_item_off, partial, num_units, out);
+  else
+    hipLaunchKernelGGL(k_unit_sumsq<64>, dim3(unsigned((num_units + 3) / 4)), dim3(256), 0, s,
+                       unit_item_off, partial, num_units, out);
   return hipGetLastError();
 }
 
-hipError_t launch_update(const UpdateArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k2_update, dim3(unsigned((a.num_units + 3) / 4)), dim3(256), 0, s, a);
+hipError_t launch_update(const UpdateArgs& a, int64_t num_items, hipStream_t s) {
+  if (a.ext_norm == nullptr && wide_units(num_items, a.num_units))
+    hipLaunchKernelGGL(k2_update<256>, dim3(unsigned(a.num_units)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(k2_update<64>, dim3(unsigned((a.num_units + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_select(const SelectArgs& a, uint64_t* keys, hipStream_t s) {
-  hipLaunchKernelGGL(k3_select, dim3(1), dim3(kK3Block), 0, s, a, keys);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k3_select, dim3(1), dim3(kK3Block), 0, s, a);
   return hipGetLastError();
 }
 

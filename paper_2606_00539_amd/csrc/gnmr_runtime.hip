@@ -184,8 +184,11 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   u.gnmr = c->d_gnmr;
   u.dgnmr = c->d_dgnmr;
   u.risk = c->d_risk;
+  u.rec = c->d_rec;
+  u.lock = c->d_lock;
+  u.keys = c->d_keys;
   u.flags = c->d_flags;
-  GNMR_HIP(gnmr::launch_update(u, st));
+  GNMR_HIP(gnmr::launch_update(u, c->num_items, st));
   gnmr_status r = record(c, 2, st);
   if (r != GNMR_OK) return r;
 
@@ -194,13 +197,12 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   s.max_o = c->max_o;
   s.lock_len = c->lock_len;
   s.t = t;
-  s.risk = c->d_risk;
   s.flags = c->d_flags;
-  s.rec = c->d_rec;
+  s.keys = c->d_keys;
   s.lock = c->d_lock;
   s.mask = c->d_mask;
   s.stats = c->d_stats;
-  GNMR_HIP(gnmr::launch_select(s, c->d_keys, st));
+  GNMR_HIP(gnmr::launch_select(s, st));
   r = record(c, 3, st);
   if (r != GNMR_OK) return r;
   c->t = t;
@@ -450,7 +452,8 @@ gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr, double* d_sums
   if (r != GNMR_OK) return r;
   GNMR_HIP(gnmr::launch_sumsq(ctx->d_items, ctx->num_items, ctx->d_seg_base, ctx->d_seg_dtype,
                               ctx->d_partial, st));
-  GNMR_HIP(gnmr::launch_unit_sumsq(ctx->d_unit_item_off, ctx->d_partial, ctx->U, d_sumsq, st));
+  GNMR_HIP(gnmr::launch_unit_sumsq(ctx->d_unit_item_off, ctx->d_partial, ctx->num_items,
+                                   ctx->U, d_sumsq, st));
   return GNMR_OK;
 }
 
