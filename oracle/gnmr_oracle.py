@@ -23,7 +23,7 @@ What it computes, per controller step t = 1, 2, ... (paper notation):
           Lock_b as left by step t-1 (Alg. 2; Sec. 3.3).
   select  A_t = Top_maxO(C_t; R): all of C_t when |C_t| <= maxO, else the
           maxO members with the largest R; maxO caps the active set, it is not
-          a quota (Alg. 2; Sec. 3.4; App. E matched-trigger setting).
+          a quota (Alg. 2; Sec. 3.4; App. E.5 matched-trigger setting).
   locks   b in A_t and R > 1 -> Lock_b = T_lock; b in A_t and R <= 1 ->
           Lock_b = max(Lock_b - 1, 0); b not in A_t -> Lock_b = 0 (Alg. 2).
 

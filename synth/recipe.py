@@ -81,7 +81,7 @@ class Workload:
 def two_stage_alpha(t: int, steps: int, hi: float = 1.5, lo: float = 1.1,
                     frac: float = 0.025) -> float:
     """Two-stage GNMR threshold: ``hi`` for the first ceil(frac * steps) steps
-    (at least one), ``lo`` afterwards (Sec. 3.4 calibration; App. C recipe
+    (at least one), ``lo`` afterwards (Sec. 3.4 calibration; App. E.2 recipe
     and 13B fine-tuning setting: 1.5 -> 1.1, first 2.5% of steps)."""
     return hi if t <= max(1, math.ceil(frac * steps)) else lo
 
