@@ -29,7 +29,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(torch, buf, lay, w, target_s: float = 10.0, max_units: int = 64):
+def cpu_baseline(torch, buf, lay, w, target_s: float = 12.0, max_units: int = 100000):
     """Oracle norm pass plus one oracle controller step, single-threaded, on a
     bounded sample of units copied off the device (copy not timed)."""
     import numpy as np
@@ -74,6 +74,45 @@ def cpu_baseline(torch, buf, lay, w, target_s: float = 10.0, max_units: int = 64
                       f"{w.bytes_per_step / 1e9:.2f} GB step"}
 
 
+def measured_traffic(workload: str):
+    """K1's HBM bytes per launch from the committed rocprofv3 counter summary,
+    or None when it is for another workload or the kernel source has changed
+    since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"k1_sumsq_{workload}_bf16_traffic.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.startswith(("|", "#", "rocprofv3")):
+            k, _, v = line.strip().partition("=")
+            kv[k] = v
+    src = b"".join(open(os.path.join(ROOT, "paper_2606_00539_amd", "csrc", f), "rb").read()
+                   for f in ("gnmr_kernels.hip", "gnmr_internal.h"))
+    if kv.get("kernel_source_sha256_16") != hashlib.sha256(src).hexdigest()[:16]:
+        return None
+    if kv.get("workload") != workload:
+        return None
+    return int(kv["fetch_bytes_per_launch"]) + int(kv["write_bytes_per_launch"])
+
+
+def copy_probe(torch, nbytes: int, steps: int, warmup: int) -> None:
+    """Device-to-device copies of nbytes (read nbytes + write nbytes each)."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    print(json.dumps({"probe": "copy", "bytes": nbytes, "ms": round(dt * 1e3, 4),
+                      "read_plus_write_GBs": round(2 * nbytes / dt / 1e9, 1)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -81,6 +120,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama2-13b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--probe-copy-bytes", type=float, default=0,
+                    help="instead of the controller, time device-to-device copies of this "
+                         "many bytes (the known-size reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -97,6 +139,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
     torch.cuda.set_device(0)
+    if args.probe_copy_bytes:
+        copy_probe(torch, int(args.probe_copy_bytes), args.steps, args.warmup)
+        return
     w = R.get(args.workload)
     lay = L.for_workload(w)
     log(f"[bench] {w.name}: {w.num_units} units, {w.bytes_per_step / 1e9:.3f} GB/step")
@@ -132,8 +177,11 @@ def main():
     gbs = w.bytes_per_step / (elapsed / args.steps) / 1e9
     k1_ms = prof["ms_sumsq"] / max(prof["steps"], 1)
     k1_gbs = w.bytes_per_step / (k1_ms * 1e-3) / 1e9
+    traffic = measured_traffic(w.name)
     roofline = {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                "algorithmic_bytes": w.bytes_per_step,
                 "kernel": "k1_sumsq", "kernel_ms": round(k1_ms, 4),
                 "update_ms": round(prof["ms_update"] / max(prof["steps"], 1), 4),
                 "select_ms": round(prof["ms_select"] / max(prof["steps"], 1), 4)}

@@ -49,10 +49,17 @@ def mix64_int(z: int) -> int:
 
 
 def mix64_np(z: np.ndarray) -> np.ndarray:
-    """SplitMix64 finaliser on a uint64 array (NumPy integer ops wrap mod 2^64)."""
-    z = (z ^ (z >> np.uint64(30))) * np.uint64(MUL1)
-    z = (z ^ (z >> np.uint64(27))) * np.uint64(MUL2)
-    return z ^ (z >> np.uint64(31))
+    """SplitMix64 finaliser on a uint64 array (NumPy integer ops wrap mod 2^64).
+    Works in place on z and returns it."""
+    t = z >> np.uint64(30)
+    z ^= t
+    z *= np.uint64(MUL1)
+    np.right_shift(z, np.uint64(27), out=t)
+    z ^= t
+    z *= np.uint64(MUL2)
+    np.right_shift(z, np.uint64(31), out=t)
+    z ^= t
+    return z
 
 
 def unit_key(seed: int, t: int, b: int) -> int:
@@ -75,15 +82,20 @@ def normal_table() -> np.ndarray:
 
 
 def table_indices(seed: int, t: int, b: int, start: int, count: int) -> np.ndarray:
-    """16-bit table indices j(i) for unit elements i in [start, start + count)."""
+    """16-bit table indices j(i) for unit elements i in [start, start + count).
+
+    One 64-bit hash serves the four elements 4g .. 4g+3; field i % 4 is the
+    (i % 4)-th 16-bit word of the hash, i.e. the little-endian uint16 view."""
     if count <= 0:
-        return np.zeros(0, dtype=np.int64)
+        return np.zeros(0, dtype=np.uint16)
+    g0, g1 = start >> 2, (start + count + 3) >> 2
     key = np.uint64(unit_key(seed, t, b))
-    i = np.arange(start, start + count, dtype=np.uint64)
-    g = (i >> np.uint64(2)) + np.uint64(1)
-    h = mix64_np(key + g * np.uint64(GAMMA))
-    shift = (i & np.uint64(3)) * np.uint64(16)
-    return ((h >> shift) & np.uint64(0xFFFF)).astype(np.int64)
+    h = np.arange(g0 + 1, g1 + 1, dtype=np.uint64)
+    h *= np.uint64(GAMMA)
+    h += key
+    words = mix64_np(h).astype("<u8", copy=False).view("<u2")
+    off = start - 4 * g0
+    return words[off:off + count]
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -101,16 +113,19 @@ def bf16_bits_to_f32(h: np.ndarray) -> np.ndarray:
 
 
 def unit_values(seed: int, t: int, b: int, scale: float, dtype: int,
-                start: int, count: int) -> np.ndarray:
+                start: int, count: int, chunk: int = 1 << 22) -> np.ndarray:
     """Elements [start, start+count) of unit b at step t.
 
     Returns float32 values for DTYPE_F32 and uint16 bf16 bit patterns for
     DTYPE_BF16 (NumPy has no bfloat16)."""
+    if dtype not in (DTYPE_F32, DTYPE_BF16):
+        raise ValueError(f"unknown dtype {dtype}")
     s = np.float32(scale)
-    z = normal_table()[table_indices(seed, t, b, start, count)]
-    x = (s * z).astype(np.float32)  # one IEEE fp32 multiply, round to nearest even
-    if dtype == DTYPE_F32:
-        return x
-    if dtype == DTYPE_BF16:
-        return f32_to_bf16_bits(x)
-    raise ValueError(f"unknown dtype {dtype}")
+    tab = normal_table()
+    out = np.empty(max(count, 0), dtype=np.float32 if dtype == DTYPE_F32 else np.uint16)
+    for lo in range(0, max(count, 0), chunk):
+        n = min(chunk, count - lo)
+        x = tab[table_indices(seed, t, b, start + lo, n)]
+        x *= s                       # one IEEE fp32 multiply, round to nearest even
+        out[lo:lo + n] = x if dtype == DTYPE_F32 else f32_to_bf16_bits(x)
+    return out

@@ -10,7 +10,7 @@ from synth import values as V
 
 def test_mix64_matches_python_ints():
     xs = np.array([0, 1, 2, 0xDEADBEEF, (1 << 64) - 1, V.GAMMA], dtype=np.uint64)
-    got = V.mix64_np(xs)
+    got = V.mix64_np(xs.copy())
     for x, g in zip(xs.tolist(), got.tolist()):
         assert V.mix64_int(int(x)) == g
 
@@ -71,3 +71,18 @@ def test_workload_shapes(name, units, numel, nbytes):
 def test_two_stage_alpha():
     assert [R.two_stage_alpha(t, 16) for t in (1, 2)] == [1.5, 1.1]
     assert [R.two_stage_alpha(t, 256) for t in (7, 8)] == [1.5, 1.1]
+
+
+@pytest.mark.parametrize("start,count", [(0, 1), (1, 7), (3, 4), (5, 1000), (1 << 20, 33)])
+def test_table_indices_match_definition(start, count):
+    # j(i) = (mix64(key + (i // 4 + 1) * GAMMA) >> (16 * (i % 4))) & 0xFFFF
+    key = V.unit_key(7, 9, 11)
+    want = [(V.mix64_int(key + (i // 4 + 1) * V.GAMMA) >> (16 * (i % 4))) & 0xFFFF
+            for i in range(start, start + count)]
+    assert V.table_indices(7, 9, 11, start, count).tolist() == want
+
+
+def test_unit_values_chunking_is_seamless():
+    a = V.unit_values(1, 2, 3, 5e-3, V.DTYPE_BF16, 5, 10_001, chunk=1 << 22)
+    b = V.unit_values(1, 2, 3, 5e-3, V.DTYPE_BF16, 5, 10_001, chunk=999)
+    assert np.array_equal(a, b)
