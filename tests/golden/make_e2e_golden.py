@@ -1,0 +1,125 @@
+"""Writes tests/golden/e2e_<workload>.npz: the oracle's expected controller
+outputs for every step of a full-size synthetic workload.
+
+Inputs come from the seeded generator (synth: the recipe, and the C host twin
+of the counter-based values).  Norms come from the oracle's plain-C float64
+sum of squares (oracle/native.py), and every step runs the oracle controller
+(oracle/gnmr_oracle.py) with the guard co-simulation of tests/streams.py,
+which nudges a unit-step's scale when a decision would sit within 1e-4 of
+its threshold.  Nothing here touches the HIP library.
+
+Stored per workload:
+  nudge_t, nudge_b, nudge_f  the nudged unit-steps (1-based step, unit, factor)
+  mask_bits    np.packbits of the [T, U] active-set masks (axis 1)
+  lock         uint8 [T, U] lock counters after each step
+  stats        int64 [T, 8] counters (t, n_trig_gnmr, n_trig_dgnmr, n_trig,
+               n_cand, n_active, hit_maxo, n_nonfinite)
+  norm32       float32 [T, U] oracle norms (float32 is far inside the 1e-5 bar)
+  sample       int64 [S] unit indices with float64 gnmr/dgnmr/risk [T, S]
+
+Usage: python tests/golden/make_e2e_golden.py [workload ...] [--threads N]
+"""
+from __future__ import annotations
+
+import argparse
+import math
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.dirname(HERE))
+
+import streams as S  # noqa: E402
+from oracle import native  # noqa: E402
+from synth import host  # noqa: E402
+from synth import recipe as R  # noqa: E402
+
+CHUNK = 1 << 22
+STAT_KEYS = ("t", "n_trig_gnmr", "n_trig_dgnmr", "n_trig", "n_cand", "n_active", "hit_maxo",
+             "n_nonfinite")
+
+
+def golden_path(name: str) -> str:
+    return os.path.join(HERE, f"e2e_{name}.npz")
+
+
+def unit_norm(seed, t, b, scale32, dtype, numel):
+    buf = np.empty(min(CHUNK, max(numel, 1)), dtype=np.float32 if dtype == 0 else np.uint16)
+    s = 0.0
+    for lo in range(0, numel, CHUNK):
+        n = min(CHUNK, numel - lo)
+        host.unit_values(seed, t, b, scale32, dtype, lo, n, out=buf[:n])
+        s += native.sumsq(buf[:n], dtype)
+    return math.sqrt(s)
+
+
+def make(name: str, threads: int) -> str:
+    w = R.get(name)
+    U, T = w.num_units, w.steps
+    pool = ThreadPoolExecutor(max_workers=threads)
+    t_start = time.time()
+
+    def norms_of_step(t, scale32, units):
+        sel = range(U) if units is None else units
+        vals = pool.map(lambda b: unit_norm(w.seed, t, b, float(scale32[b]), w.units[b].dtype,
+                                            w.units[b].numel), sel)
+        out = dict(zip(sel, vals))
+        if units is None:
+            print(f"  {name} t={t}/{T} ({time.time() - t_start:.0f} s)", flush=True)
+        return out
+
+    nudge, norms, res, _, _ = S.guarded_stream(w, norms_of_step)
+    pool.shutdown()
+    masks = np.stack([r.mask for r in res]).astype(np.uint8)
+    locks = np.stack([r.lock for r in res])
+    assert locks.max() <= 255
+    stats = np.array([[r.stats[k] for k in STAT_KEYS] for r in res], dtype=np.int64)
+    rng = np.random.default_rng(7)
+    ever = np.flatnonzero(masks.any(axis=0))
+    sample = np.unique(np.concatenate([
+        np.arange(U) if U <= 300 else rng.choice(U, 192, replace=False),
+        ever[:64], [0, U - 1]])).astype(np.int64)
+    nt, nb = np.nonzero(nudge != 1.0)
+    out = golden_path(name)
+    np.savez_compressed(
+        out, workload=name, steps=T, units=U,
+        nudge_t=(nt + 1).astype(np.int64), nudge_b=nb.astype(np.int64),
+        nudge_f=nudge[nt, nb],
+        mask_bits=np.packbits(masks, axis=1), lock=locks.astype(np.uint8), stats=stats,
+        norm32=norms.astype(np.float32), sample=sample,
+        gnmr=np.stack([r.gnmr[sample] for r in res]),
+        dgnmr=np.stack([r.dgnmr[sample] for r in res]),
+        risk=np.stack([r.risk[sample] for r in res]))
+    print(f"{name}: {T} steps x {U} units, {len(nt)} nudged unit-steps, "
+          f"{int(masks.sum())} active unit-steps, {time.time() - t_start:.0f} s -> {out}",
+          flush=True)
+    return out
+
+
+def load(name: str) -> dict:
+    z = np.load(golden_path(name), allow_pickle=False)
+    d = {k: z[k] for k in z.files}
+    d["mask"] = np.unpackbits(d["mask_bits"], axis=1, count=int(d["units"])).astype(np.uint8)
+    return d
+
+
+def nudge_table(d: dict) -> np.ndarray:
+    nudge = np.ones((int(d["steps"]), int(d["units"])))
+    nudge[d["nudge_t"] - 1, d["nudge_b"]] = d["nudge_f"]
+    return nudge
+
+
+if __name__ == "__main__":
+    ap = argparse.ArgumentParser()
+    ap.add_argument("workloads", nargs="*",
+                    default=["tiny", "llama2-7b", "llama2-13b", "moe", "fine128", "fine32"])
+    ap.add_argument("--threads", type=int, default=os.cpu_count() or 8)
+    a = ap.parse_args()
+    for n in a.workloads:
+        make(n, a.threads)

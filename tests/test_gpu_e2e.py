@@ -1,0 +1,73 @@
+"""End-to-end parity on every step of every workload, at full size.
+
+The expected outputs (tests/golden/e2e_<workload>.npz) were written by
+tests/golden/make_e2e_golden.py from the oracle alone: host-generated
+gradients, the oracle's float64 norms and controller, and guard nudges that
+keep every decision at least 1e-4 from its threshold.  Here the same
+gradients are generated on the device (the HIP generator is bit-identical to
+the host twin) and run through gnmr_step in the benchmark's launch
+configuration.  Masks, locks and counters must match bit for bit; norms (all
+units) and GNMR, Delta-GNMR and R (a stored sample of units) within 1e-5.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from golden.make_e2e_golden import golden_path, load, nudge_table
+from gpu_util import controller_for, device_buffer, require_gpu
+from synth import layout as L
+from synth import recipe as R
+
+pytestmark = pytest.mark.gpu
+
+E2E = ["tiny", "llama2-7b", "llama2-13b", "moe", "fine128", "fine32"]
+STAT_KEYS = ("t", "n_trig_gnmr", "n_trig_dgnmr", "n_trig", "n_cand", "n_active", "hit_maxo",
+             "n_nonfinite")
+
+
+@pytest.fixture(scope="module")
+def gen():
+    require_gpu()
+    from synth.gpu import Generator
+
+    return Generator()
+
+
+@pytest.mark.parametrize("name", E2E)
+def test_e2e_every_step_matches_oracle(gen, name):
+    torch = require_gpu()
+    d = load(name)
+    w = R.get(name)
+    assert int(d["units"]) == w.num_units and int(d["steps"]) == w.steps
+    nudge = nudge_table(d)
+    sample = d["sample"]
+    lay = L.for_workload(w)
+    print(f"e2e {name}: {w.steps} steps x {w.num_units} units, "
+          f"{len(d['nudge_t'])} nudged unit-steps ({golden_path(name)})", flush=True)
+    sys.stdout.flush()
+    buf, base, ptrs = device_buffer(torch, lay)
+    active = 0
+    try:
+        with controller_for(lay, w, ptrs) as ctl:
+            for t in range(1, w.steps + 1):
+                gen.fill(lay, base, w.seed, t, w.scale32(t, nudge[t - 1]))
+                ctl.step(w.alpha(t), w.beta(t))
+                out = ctl.query()
+                what = f"{name} t={t}"
+                bad = np.flatnonzero(out["mask"] != d["mask"][t - 1])
+                assert bad.size == 0, f"{what}: mask differs at units {bad[:10]}"
+                bad = np.flatnonzero(out["lock"] != d["lock"][t - 1])
+                assert bad.size == 0, f"{what}: lock differs at units {bad[:10]}"
+                got = [out["stats"][k] for k in STAT_KEYS]
+                assert got == d["stats"][t - 1].tolist(), f"{what}: stats {got}"
+                np.testing.assert_allclose(out["norm"], d["norm32"][t - 1], rtol=1e-5, atol=0,
+                                           err_msg=f"{what} norm")
+                for f in ("gnmr", "dgnmr", "risk"):
+                    np.testing.assert_allclose(out[f][sample], d[f][t - 1], rtol=1e-5, atol=0,
+                                               err_msg=f"{what} {f}")
+                active += int(out["mask"].sum())
+        print(f"  {name}: all {w.steps} steps match, {active} active unit-steps", flush=True)
+    finally:
+        del buf
+        torch.cuda.empty_cache()

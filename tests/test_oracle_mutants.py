@@ -1,0 +1,97 @@
+"""Strength of the oracle pins: plausible mistakes are planted into a copy of
+the oracle (on the CPU, never in the real one) and at least one pin must fail
+for each.  CPU only."""
+import importlib.util
+import os
+import sys
+import types
+
+import pytest
+
+import test_oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle",
+                   "gnmr_oracle.py")
+
+# (name, original text, planted mistake)
+MUTANTS = [
+    ("running mean over t+1", "A_next = self.A + (n - self.A) / t",
+     "A_next = self.A + (n - self.A) / (t + 1)"),
+    ("window mean over delta+1", "den = total / delta + eps", "den = total / (delta + 1) + eps"),
+    ("eps subtracted", "n[has_mean] / (self.A[has_mean] + eps)",
+     "n[has_mean] / (self.A[has_mean] - eps)"),
+    ("eps dropped from window", "den = total / delta + eps", "den = total / delta"),
+    ("queue keeps delta+1", "if len(self.Q) > delta:", "if len(self.Q) > delta + 1:"),
+    ("min instead of max", "risk = np.maximum(g_term, d_term)", "risk = np.minimum(g_term, d_term)"),
+    ("alpha and beta swapped", "g_term = gnmr / alpha", "g_term = gnmr / beta"),
+    ("non-strict trigger", "triggered = self.rec & (risk > 1.0)",
+     "triggered = self.rec & (risk >= 1.0)"),
+    ("locks ignored in pool", "cand = triggered | (self.rec & (self.lock > 0))",
+     "cand = triggered"),
+    ("non-recoverable selectable", "triggered = self.rec & (risk > 1.0)",
+     "triggered = (risk > 1.0)"),
+    ("ascending selection", "order = np.lexsort((cand_idx, -risk[cand_idx]))",
+     "order = np.lexsort((cand_idx, risk[cand_idx]))"),
+    ("ties to larger index", "order = np.lexsort((cand_idx, -risk[cand_idx]))",
+     "order = np.lexsort((-cand_idx, -risk[cand_idx]))"),
+    ("lock set to T_lock - 1", "new_lock[b] = self.lock_len", "new_lock[b] = self.lock_len - 1"),
+    ("lock not decremented", "new_lock[b] = max(self.lock[b] - 1, 0)",
+     "new_lock[b] = max(self.lock[b], 0)"),
+    ("eviction keeps lock", "new_lock = np.zeros(U, dtype=np.int64)", "new_lock = self.lock.copy()"),
+    ("budget off by one", "if cand_idx.size <= self.max_o:", "if cand_idx.size <= self.max_o + 1:"),
+    ("L1 instead of L2", "s += float(np.dot(x, x))", "s += float(np.sum(np.abs(x)))"),
+    ("bf16 widened wrongly", "<< np.uint32(16)", "<< np.uint32(15)"),
+    ("GNMR not clamped at A = 0", "has_mean = finite & (self.A != 0.0)", "has_mean = finite"),
+    ("current GNMR in window", "for q in self.Q:                       # oldest to newest",
+     "for q in self.Q[1:] + [gnmr]:"),
+]
+
+PINS = [
+    (P.test_sumsq_matches_exact_rational, dict(dtype=P.BF16)),
+    (P.test_norm_of_constant_magnitude_is_closed_form, {}),
+    (P.test_gnmr_and_dgnmr_follow_definitions, dict(delta=3)),
+    (P.test_running_mean_is_arithmetic_mean, {}),
+    (P.test_constant_magnitude_gives_exact_ones, {}),
+    (P.test_spike_closed_form, dict(k=20, t0=7)),
+    (P.test_zero_mean_rules, {}),
+    (P.test_selection_equals_brute_force_and_invariants, dict(seed=0)),
+    (P.test_selection_equals_brute_force_and_invariants, dict(seed=3)),
+    (P.test_lock_holds_exactly_lock_len_steps, dict(lock_len=4)),
+    (P.test_eviction_clears_lock, {}),
+    (P.test_alpha_below_one_is_pure_top_k, {}),
+    (P.test_non_recoverable_units_are_monitored_only, {}),
+    (P.test_eps_enters_both_denominators, {}),
+    (P.test_trigger_is_strict, {}),
+]
+
+
+def mutant_module(original: str, planted: str) -> types.ModuleType:
+    src = open(SRC).read()
+    assert original in src, f"mutation anchor not found: {original!r}"
+    spec = importlib.util.spec_from_loader("oracle_mutant", loader=None)
+    mod = importlib.util.module_from_spec(spec)
+    sys.modules["oracle_mutant"] = mod          # dataclasses look the module up
+    try:
+        exec(compile(src.replace(original, planted, 1), "oracle_mutant", "exec"), mod.__dict__)
+    finally:
+        del sys.modules["oracle_mutant"]
+    return mod
+
+
+@pytest.mark.parametrize("name,original,planted", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(monkeypatch, name, original, planted):
+    mod = mutant_module(original, planted)
+    for attr in ("Controller", "sumsq", "unit_norm"):
+        monkeypatch.setattr(P, attr, getattr(mod, attr))
+    caught = []
+    for fn, kw in PINS:
+        try:
+            fn(**kw)
+        except (AssertionError, ValueError, IndexError, ZeroDivisionError, FloatingPointError):
+            caught.append(fn.__name__)
+    assert caught, f"no pin fails for the planted mistake: {name}"
+
+
+def test_unmutated_oracle_passes_every_listed_pin():
+    for fn, kw in PINS:
+        fn(**kw)

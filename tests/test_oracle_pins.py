@@ -365,3 +365,41 @@ def test_invalid_arguments_raise():
         ctl.step([1, 1, 1], 0.0, 1.5)
     with pytest.raises(ValueError):
         ctl.step([1, 1, 1], 1.1, float("nan"))
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+def test_native_sumsq_matches_exact_rational_and_numpy(dtype):
+    from oracle import native
+
+    x = V.unit_values(seed=4, t=2, b=1, scale=2.3e-3, dtype=dtype, start=3, count=4001)
+    f = V.bf16_bits_to_f32(x) if dtype == BF16 else x
+    exact = sum((Fraction(float(v)) ** 2 for v in f), Fraction(0))
+    got = native.sumsq(x, dtype)
+    assert rel(got, exact) < 4001 * 1.2e-16
+    big = V.unit_values(seed=4, t=2, b=2, scale=2.3e-3, dtype=dtype, start=0, count=3_000_001)
+    assert rel(native.sumsq(big, dtype), sumsq([(big, dtype)])) < 1e-10
+
+
+def test_eps_enters_both_denominators():
+    # GNMR_t = n_t / (A_{t-1} + eps), Delta_t = GNMR_t / (mean(Q) + eps) (Alg. 1),
+    # checked with a large eps in exact rationals.
+    eps, delta = 0.5, 2
+    norms = [1.0, 3.0, 2.0, 4.0, 1.5]
+    ctl = Controller(1, window=delta, max_o=1, lock_len=1, eps=eps)
+    A, Q = Fraction(0), []
+    for t, n in enumerate(norms, start=1):
+        r = ctl.step([n], 1.1, 1.5)
+        G = Fraction(1) if (t == 1 or A == 0) else Fraction(n) / (A + Fraction(eps))
+        D = G / (sum(Q, Fraction(0)) / delta + Fraction(eps)) if len(Q) == delta else Fraction(1)
+        assert rel(r.gnmr[0], G) < 1e-15 and rel(r.dgnmr[0], D) < 1e-15
+        A = A + (Fraction(n) - A) / t
+        Q = (Q + [G])[-delta:]
+
+
+def test_trigger_is_strict():
+    # constant magnitude with alpha = 1: R = GNMR / alpha = 1 exactly, which is
+    # not a trigger (Alg. 2 uses R > 1)
+    ctl = Controller(2, window=3, max_o=2, lock_len=2, eps=0.0)
+    for t in range(10):
+        r = ctl.step([0.25, 4.0], 1.0, 1.0)
+        assert np.all(r.risk == 1.0) and r.mask.sum() == 0 and r.stats["n_trig"] == 0

@@ -86,3 +86,13 @@ def test_unit_values_chunking_is_seamless():
     a = V.unit_values(1, 2, 3, 5e-3, V.DTYPE_BF16, 5, 10_001, chunk=1 << 22)
     b = V.unit_values(1, 2, 3, 5e-3, V.DTYPE_BF16, 5, 10_001, chunk=999)
     assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("dtype", [V.DTYPE_F32, V.DTYPE_BF16])
+@pytest.mark.parametrize("start,count", [(0, 1), (2, 9), (7, 100_003), (1 << 24, 4)])
+def test_c_twin_is_bit_identical(dtype, start, count):
+    from synth import host
+
+    a = V.unit_values(3, 17, 123, 7.7e-4, dtype, start, count)
+    b = host.unit_values(3, 17, 123, 7.7e-4, dtype, start, count)
+    assert a.dtype == b.dtype and np.array_equal(a, b)
