@@ -26,6 +26,16 @@ struct Item {
 };
 static_assert(sizeof(Item) == 16, "Item layout");
 
+// Step counters accumulated by K2 (integer atomics) and read by K3.
+enum : int {
+  kCntCand = 0,       // |C_t|
+  kCntTrigG = 1,      // recoverable units with GNMR / alpha > 1
+  kCntTrigD = 2,      // recoverable units with Delta-GNMR / beta > 1
+  kCntTrigR = 3,      // recoverable units with R > 1
+  kCntNonFinite = 4,  // units with a non-finite norm
+  kNumCounters = 8
+};
+
 // Per-unit flag bits written by K2 and read by K3.
 enum : uint8_t {
   kFlagTrigG = 1,      // GNMR / alpha > 1
@@ -53,9 +63,12 @@ struct UpdateArgs {
   double* dgnmr;
   double* risk;
   const uint8_t* rec;            // [U]
-  const int32_t* lock;           // [U], Lock after step t-1
+  int32_t* lock;                 // [U], Lock after step t-1 (cleared for units outside C_t)
   uint64_t* keys;                // [U], candidate key or 0
   uint8_t* flags;
+  uint8_t* mask;                 // [U], cleared for units outside C_t
+  int32_t* counters;             // [kNumCounters], zero on entry
+  int32_t* cand_list;            // [U], members of C_t (any order), counters[kCntCand] of them
 };
 
 struct SelectArgs {
@@ -65,6 +78,8 @@ struct SelectArgs {
   int64_t t;
   const uint8_t* flags;
   const uint64_t* keys;
+  int32_t* counters;         // from K2; reset to zero for the next step
+  const int32_t* cand_list;  // from K2
   int32_t* lock;       // in: Lock after step t-1; out: after step t
   uint8_t* mask;
   gnmr_stats* stats;

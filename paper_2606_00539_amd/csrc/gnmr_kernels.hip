@@ -166,7 +166,8 @@ __global__ __launch_bounds__(kK1Block) void k1_sumsq(const Item* __restrict__ it
 
 // Fixed-order float64 sum of unit b's item partials by L lanes (lane < L):
 // each lane keeps four running sums over a stride-L walk, then the lanes are
-// combined by a fixed butterfly (and, for L = 256, a fixed cross-wave order).
+// combined by a fixed butterfly (L = 64) and a fixed cross-wave order
+// (L = 256).  L = 1 is one thread per unit, for units of few items.
 template <int L>
 __device__ __forceinline__ double unit_ss(const int64_t* __restrict__ off,
                                           const float* __restrict__ partial, int b, int lane,
@@ -182,12 +183,15 @@ __device__ __forceinline__ double unit_ss(const int64_t* __restrict__ off,
     s3 += double(e);
   }
   for (; i < hi; i += L) s0 += double(partial[i]);
-  double s = wave_sum((s0 + s1) + (s2 + s3));
-  if constexpr (L == 64) {
+  const double s = (s0 + s1) + (s2 + s3);
+  if constexpr (L == 1) {
     return s;
+  } else if constexpr (L == 64) {
+    return wave_sum(s);
   } else {
-    static_assert(L == 256, "64 or 256 lanes per unit");
-    if ((lane & 63) == 0) red[lane >> 6] = s;
+    static_assert(L == 256, "1, 64 or 256 lanes per unit");
+    const double w = wave_sum(s);
+    if ((lane & 63) == 0) red[lane >> 6] = w;
     __syncthreads();
     return ((red[0] + red[1]) + red[2]) + red[3];
   }
@@ -198,7 +202,7 @@ __global__ __launch_bounds__(256) void k_unit_sumsq(const int64_t* __restrict__ 
                                                     const float* __restrict__ partial,
                                                     int num_units, double* __restrict__ out) {
   __shared__ double red[4];
-  const int lane = threadIdx.x % L;
+  const int lane = L == 1 ? 0 : int(threadIdx.x % L);
   const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
   if (b >= num_units) return;  // uniform per workgroup when L = 256
   const double s = unit_ss<L>(off, partial, b, lane, red);
@@ -216,7 +220,7 @@ __device__ __forceinline__ uint64_t cand_key(double R) {
 template <int L>
 __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   __shared__ double red[4];
-  const int lane = threadIdx.x % L;
+  const int lane = L == 1 ? 0 : int(threadIdx.x % L);
   const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
   if (b >= a.num_units) return;  // uniform per workgroup when L = 256
   double n;
@@ -258,6 +262,7 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   const bool rec = a.rec[b] != 0;
   const bool trig = R > 1.0;
   const bool cand = rec && (trig || a.lock[b] > 0);
+  const bool tg = rec && gt > 1.0, td = rec && dt > 1.0, tr = rec && trig;
   a.norm[b] = n;
   a.gnmr[b] = G;
   a.dgnmr[b] = D;
@@ -266,9 +271,42 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   a.flags[b] = uint8_t((gt > 1.0 ? kFlagTrigG : 0) | (dt > 1.0 ? kFlagTrigD : 0) |
                        (finite ? 0 : kFlagNonFinite) | (trig ? kFlagTrigR : 0) |
                        (rec ? kFlagRec : 0) | (cand ? kFlagCand : 0));
+  // Alg. 2 outcome of a unit outside C_t is fixed already: low-cost path,
+  // Lock = 0.  K3 only has to rank and update the members of C_t.
+  if (!cand) {
+    a.mask[b] = 0;
+    if (a.lock[b] != 0) a.lock[b] = 0;
+  }
+  // Counters and the list of C_t (integer atomics: exact; list order is
+  // irrelevant to the selection).
+  if constexpr (L == 1) {
+    const uint64_t active = __ballot(1);
+    const int leader = __ffsll((unsigned long long)active) - 1;
+    const int wl = threadIdx.x & 63;
+    const uint64_t m_c = __ballot(cand);
+    const uint64_t m_g = __ballot(tg), m_d = __ballot(td), m_r = __ballot(tr);
+    const uint64_t m_n = __ballot(!finite);
+    int base = 0;
+    if (wl == leader) {
+      if (m_c) base = atomicAdd(&a.counters[kCntCand], __popcll(m_c));
+      if (m_g) atomicAdd(&a.counters[kCntTrigG], __popcll(m_g));
+      if (m_d) atomicAdd(&a.counters[kCntTrigD], __popcll(m_d));
+      if (m_r) atomicAdd(&a.counters[kCntTrigR], __popcll(m_r));
+      if (m_n) atomicAdd(&a.counters[kCntNonFinite], __popcll(m_n));
+    }
+    base = __shfl(base, leader, 64);
+    if (cand) a.cand_list[base + __popcll(m_c & ((uint64_t(1) << wl) - 1))] = b;
+  } else {
+    if (cand) a.cand_list[atomicAdd(&a.counters[kCntCand], 1)] = b;
+    if (tg) atomicAdd(&a.counters[kCntTrigG], 1);
+    if (td) atomicAdd(&a.counters[kCntTrigD], 1);
+    if (tr) atomicAdd(&a.counters[kCntTrigR], 1);
+    if (!finite) atomicAdd(&a.counters[kCntNonFinite], 1);
+  }
 }
 
 constexpr int kK3Block = 1024;
+constexpr int kK3Cap = 4096;  // candidates held in LDS; larger pools use the global keys
 
 // Lock update of Alg. 2 for one unit given its selection.
 __device__ __forceinline__ void apply_selection(const SelectArgs& a, int b, bool sel, uint8_t f) {
@@ -281,122 +319,185 @@ __device__ __forceinline__ void apply_selection(const SelectArgs& a, int b, bool
   a.mask[b] = sel ? 1 : 0;
 }
 
-// K3: a single workgroup.  When |C_t| <= maxO every candidate is active.
-// Otherwise Top_maxO is a radix select over the 64-bit keys (8 passes of 8
-// bits, most significant first) for the maxO-th largest key T; every
-// candidate with key > T is active, and the first `need` candidates with
-// key == T in index order.
-__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
-  __shared__ int cnt[6];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t scan[kK3Block];
-  __shared__ int s_digit, s_k;
+// MSB-first radix select, 8 passes of 8 bits: the k-th largest (1-based) of
+// the n keys key_at(i), i < n.  Returns it as T; *rest receives how many keys
+// equal to T are among the k largest.  Called by every thread of the
+// workgroup.
+template <typename KeyAt>
+__device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int* s_digit,
+                                 int* s_k, int* rest) {
+  const int tid = threadIdx.x;
+  uint64_t prefix = 0, pmask = 0;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += kK3Block) {
+      const uint64_t key = key_at(i);
+      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t cum = 0;
+      int d = 255;
+      for (; d > 0; --d) {
+        if (cum + hist[d] >= uint32_t(k)) break;
+        cum += hist[d];
+      }
+      *s_digit = d;
+      *s_k = k - int(cum);
+    }
+    __syncthreads();
+    prefix |= uint64_t(*s_digit) << shift;
+    pmask |= uint64_t(255) << shift;
+    k = *s_k;
+    __syncthreads();
+  }
+  *rest = k;
+  return prefix;
+}
+
+// Selection over every unit from the global keys: key > T, or key == T and
+// among the first `need` such units in index order (contiguous index ranges
+// per thread and an exclusive scan of their tie counts).
+__device__ int select_by_scan(const SelectArgs& a, uint64_t T, int need, uint32_t* scan) {
   const int tid = threadIdx.x;
   const int U = a.num_units;
-  if (tid < 6) cnt[tid] = 0;
+  const int per = (U + kK3Block - 1) / kK3Block;
+  const int lo = tid * per < U ? tid * per : U;
+  const int hi = lo + per < U ? lo + per : U;
+  uint32_t ties = 0;
+  for (int b = lo; b < hi; ++b) ties += a.keys[b] == T;
+  scan[tid] = ties;
   __syncthreads();
-
-  int c_cand = 0, c_tg = 0, c_td = 0, c_tr = 0, c_nf = 0;
-  for (int b = tid; b < U; b += kK3Block) {
-    const uint8_t f = a.flags[b];
-    c_cand += (f & kFlagCand) != 0;
-    if (f & kFlagRec) {
-      c_tg += (f & kFlagTrigG) != 0;
-      c_td += (f & kFlagTrigD) != 0;
-      c_tr += (f & kFlagTrigR) != 0;
-    }
-    c_nf += (f & kFlagNonFinite) != 0;
+  for (int d = 1; d < kK3Block; d <<= 1) {
+    const uint32_t v = tid >= d ? scan[tid - d] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
   }
-  if (c_cand) atomicAdd(&cnt[0], c_cand);
-  if (c_tg) atomicAdd(&cnt[1], c_tg);
-  if (c_td) atomicAdd(&cnt[2], c_td);
-  if (c_tr) atomicAdd(&cnt[3], c_tr);
-  if (c_nf) atomicAdd(&cnt[4], c_nf);
+  uint32_t rank = scan[tid] - ties;  // ties before this thread's range
+  int c_act = 0;
+  for (int b = lo; b < hi; ++b) {
+    const uint64_t key = a.keys[b];
+    bool sel = key > T;
+    if (key == T) {
+      sel = rank < uint32_t(need);
+      ++rank;
+    }
+    apply_selection(a, b, sel, a.flags[b]);
+    c_act += sel;
+  }
+  return c_act;
+}
+
+// Ascending bitonic sort of v[0..kK3Block) in LDS by the whole workgroup.
+__device__ void bitonic_sort(int32_t* v) {
+  const int tid = threadIdx.x;
+  for (int size = 2; size <= kK3Block; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      const int j = tid ^ stride;
+      if (j > tid) {
+        const bool up = (tid & size) == 0;
+        const int32_t x = v[tid], y = v[j];
+        if ((x > y) == up) {
+          v[tid] = y;
+          v[j] = x;
+        }
+      }
+    }
+  }
   __syncthreads();
-  const int n_cand = cnt[0];
+}
+
+// K3: a single workgroup, over the members of C_t listed by K2.  When
+// |C_t| <= maxO every candidate is active.  Otherwise Top_maxO needs the
+// maxO-th largest key T (radix select): every candidate with key > T is
+// active, and the first `need` candidates with key == T in index order.
+// Pools of up to kK3Cap candidates are ranked in LDS; larger ones over the
+// global keys of all units.
+__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
+  __shared__ uint64_t c_key[kK3Cap];
+  __shared__ int32_t c_idx[kK3Cap];
+  __shared__ int32_t tie_idx[kK3Block];
+  __shared__ uint32_t hist[256];
+  __shared__ int cnt[2];  // active, ties
+  __shared__ int s_digit, s_k;
+  uint32_t* scan = reinterpret_cast<uint32_t*>(tie_idx);  // the global path reuses it
+  const int tid = threadIdx.x;
+  const int U = a.num_units;
+  const int n_cand = a.counters[kCntCand];
+  if (tid < 2) cnt[tid] = 0;
+  __syncthreads();
 
   int c_act = 0;
   if (a.max_o == 0 || n_cand <= a.max_o) {
     // A_t = C_t (or empty when maxO = 0): no ranking needed.
     const bool take = a.max_o > 0;
-    for (int b = tid; b < U; b += kK3Block) {
-      const uint8_t f = a.flags[b];
-      const bool sel = take && (f & kFlagCand);
-      apply_selection(a, b, sel, f);
-      c_act += sel;
+    for (int i = tid; i < n_cand; i += kK3Block) {
+      const int b = a.cand_list[i];
+      apply_selection(a, b, take, a.flags[b]);
+      c_act += take;
     }
-  } else {
+  } else if (n_cand > kK3Cap) {
+    int need = 0;
     const uint64_t* __restrict__ keys = a.keys;
-    uint64_t prefix = 0, pmask = 0;
-    int k = a.max_o;  // rank of T from the top, 1-based
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      if (tid < 256) hist[tid] = 0;
-      __syncthreads();
-      for (int b = tid; b < U; b += kK3Block) {
-        const uint64_t key = keys[b];
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      if (tid == 0) {
-        uint32_t cum = 0;
-        int d = 255;
-        for (; d > 0; --d) {
-          if (cum + hist[d] >= uint32_t(k)) break;
-          cum += hist[d];
-        }
-        s_digit = d;
-        s_k = k - int(cum);
-      }
-      __syncthreads();
-      prefix |= uint64_t(s_digit) << shift;
-      pmask |= uint64_t(255) << shift;
-      k = s_k;
-      __syncthreads();
+    const uint64_t T = radix_select([=](int i) { return keys[i]; }, U, a.max_o, hist, &s_digit,
+                                    &s_k, &need);
+    c_act = select_by_scan(a, T, need, scan);
+  } else {
+    for (int i = tid; i < n_cand; i += kK3Block) {
+      const int b = a.cand_list[i];
+      c_idx[i] = b;
+      c_key[i] = a.keys[b];
     }
-    const uint64_t T = prefix;  // >= 1: more than maxO keys are >= 1
-    const int need = k;         // keys equal to T to take, in index order
-
-    // Contiguous index ranges per thread, so that ties at T are ranked in
-    // index order by an exclusive scan of per-thread tie counts.
-    const int per = (U + kK3Block - 1) / kK3Block;
-    const int lo = tid * per < U ? tid * per : U;
-    const int hi = lo + per < U ? lo + per : U;
-    uint32_t ties = 0;
-    for (int b = lo; b < hi; ++b) ties += keys[b] == T;
-    scan[tid] = ties;
     __syncthreads();
-    for (int d = 1; d < kK3Block; d <<= 1) {
-      const uint32_t v = tid >= d ? scan[tid - d] : 0;
-      __syncthreads();
-      scan[tid] += v;
-      __syncthreads();
-    }
-    uint32_t rank = scan[tid] - ties;  // ties before this thread's range
-    for (int b = lo; b < hi; ++b) {
-      const uint64_t key = keys[b];
-      bool sel = key > T;
-      if (key == T) {
-        sel = rank < uint32_t(need);
-        ++rank;
+    int need = 0;
+    const uint64_t T = radix_select([&](int i) { return c_key[i]; }, n_cand, a.max_o, hist,
+                                    &s_digit, &s_k, &need);
+    // Ties at T: gather their indices; when more tie than may be taken, keep
+    // the `need` smallest indices, i.e. every tie with index <= cut.
+    for (int i = tid; i < n_cand; i += kK3Block) {
+      if (c_key[i] == T) {
+        const int slot = atomicAdd(&cnt[1], 1);
+        if (slot < kK3Block) tie_idx[slot] = c_idx[i];
       }
-      apply_selection(a, b, sel, a.flags[b]);
-      c_act += sel;
+    }
+    __syncthreads();
+    const int n_ties = cnt[1];
+    if (n_ties > kK3Block) {
+      c_act = select_by_scan(a, T, need, scan);
+    } else {
+      int32_t cut = INT32_MAX;  // every tie taken
+      if (n_ties > need) {
+        if (tid >= n_ties) tie_idx[tid] = INT32_MAX;
+        bitonic_sort(tie_idx);
+        cut = tie_idx[need - 1];
+      }
+      for (int i = tid; i < n_cand; i += kK3Block) {
+        const int b = c_idx[i];
+        const uint64_t key = c_key[i];
+        const bool sel = key > T || (key == T && b <= cut);
+        apply_selection(a, b, sel, a.flags[b]);
+        c_act += sel;
+      }
     }
   }
-  if (c_act) atomicAdd(&cnt[5], c_act);
+  if (c_act) atomicAdd(&cnt[0], c_act);
   __syncthreads();
   if (tid == 0) {
     gnmr_stats st;
     st.t = a.t;
-    st.n_trig_gnmr = cnt[1];
-    st.n_trig_dgnmr = cnt[2];
-    st.n_trig = cnt[3];
+    st.n_trig_gnmr = a.counters[kCntTrigG];
+    st.n_trig_dgnmr = a.counters[kCntTrigD];
+    st.n_trig = a.counters[kCntTrigR];
     st.n_cand = n_cand;
-    st.n_active = cnt[5];
+    st.n_active = cnt[0];
     st.hit_maxo = (n_cand > 0 && n_cand >= a.max_o) ? 1 : 0;
-    st.n_nonfinite = cnt[4];
+    st.n_nonfinite = a.counters[kCntNonFinite];
     st.reserved = 0;
     *a.stats = st;
+    for (int k = 0; k < kNumCounters; ++k) a.counters[k] = 0;  // ready for the next step
   }
 }
 
@@ -410,28 +511,45 @@ hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const*
   return hipGetLastError();
 }
 
-// Lanes per unit for the partial sums: a whole workgroup once a unit has
-// many items (long strided walks are latency bound), else one wavefront.
-static bool wide_units(const int64_t num_items, int32_t num_units) {
-  return num_items >= int64_t(num_units) * 512;
+// Lanes per unit for the partial sums: one thread when units have few items,
+// a wavefront for moderate counts, a whole workgroup once long strided walks
+// would be latency bound.
+static int lanes_per_unit(int64_t num_items, int32_t num_units) {
+  const int64_t per = num_items / (num_units > 0 ? num_units : 1);
+  return per < 16 ? 1 : per < 512 ? 64 : 256;
+}
+
+template <int L>
+static dim3 unit_grid(int32_t num_units) {
+  return dim3(unsigned((int64_t(num_units) * L + 255) / 256));
 }
 
 hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,
                              int64_t num_items, int32_t num_units, double* out, hipStream_t s) {
-  if (wide_units(num_items, num_units))
-    hipLaunchKernelGGL(k_unit_sumsq<256>, dim3(unsigned(num_units)), dim3(256), 0, s,
-                       unit_item_off, partial, num_units, out);
-  else
-    hipLaunchKernelGGL(k_unit_sumsq<64>, dim3(unsigned((num_units + 3) / 4)), dim3(256), 0, s,
-                       unit_item_off, partial, num_units, out);
+  switch (lanes_per_unit(num_items, num_units)) {
+    case 1:
+      hipLaunchKernelGGL(k_unit_sumsq<1>, unit_grid<1>(num_units), dim3(256), 0, s,
+                         unit_item_off, partial, num_units, out);
+      break;
+    case 64:
+      hipLaunchKernelGGL(k_unit_sumsq<64>, unit_grid<64>(num_units), dim3(256), 0, s,
+                         unit_item_off, partial, num_units, out);
+      break;
+    default:
+      hipLaunchKernelGGL(k_unit_sumsq<256>, unit_grid<256>(num_units), dim3(256), 0, s,
+                         unit_item_off, partial, num_units, out);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_update(const UpdateArgs& a, int64_t num_items, hipStream_t s) {
-  if (a.ext_norm == nullptr && wide_units(num_items, a.num_units))
-    hipLaunchKernelGGL(k2_update<256>, dim3(unsigned(a.num_units)), dim3(256), 0, s, a);
+  const int L = a.ext_norm != nullptr ? 1 : lanes_per_unit(num_items, a.num_units);
+  if (L == 1)
+    hipLaunchKernelGGL(k2_update<1>, unit_grid<1>(a.num_units), dim3(256), 0, s, a);
+  else if (L == 64)
+    hipLaunchKernelGGL(k2_update<64>, unit_grid<64>(a.num_units), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(k2_update<64>, dim3(unsigned((a.num_units + 3) / 4)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k2_update<256>, unit_grid<256>(a.num_units), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

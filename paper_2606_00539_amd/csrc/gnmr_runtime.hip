@@ -95,6 +95,8 @@ struct gnmr_ctx {
   uint8_t* d_flags = nullptr;
   uint8_t* d_mask = nullptr;
   uint64_t* d_keys = nullptr;
+  int32_t* d_counters = nullptr;
+  int32_t* d_cand_list = nullptr;
   gnmr_stats* d_stats = nullptr;
 
   // pinned staging for segment-pointer uploads; `upload_done` guards reuse
@@ -188,6 +190,9 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   u.lock = c->d_lock;
   u.keys = c->d_keys;
   u.flags = c->d_flags;
+  u.mask = c->d_mask;
+  u.counters = c->d_counters;
+  u.cand_list = c->d_cand_list;
   GNMR_HIP(gnmr::launch_update(u, c->num_items, st));
   gnmr_status r = record(c, 2, st);
   if (r != GNMR_OK) return r;
@@ -199,6 +204,8 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   s.t = t;
   s.flags = c->d_flags;
   s.keys = c->d_keys;
+  s.counters = c->d_counters;
+  s.cand_list = c->d_cand_list;
   s.lock = c->d_lock;
   s.mask = c->d_mask;
   s.stats = c->d_stats;
@@ -319,6 +326,8 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   const size_t o_fl = take(size_t(U));
   const size_t o_mask = take(size_t(U));
   const size_t o_keys = take(size_t(U) * sizeof(uint64_t));
+  const size_t o_cnt = take(gnmr::kNumCounters * sizeof(int32_t));
+  const size_t o_list = take(size_t(U) * sizeof(int32_t));
   const size_t o_st = take(sizeof(gnmr_stats));
   const size_t total = off;
 
@@ -349,6 +358,8 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   c->d_flags = reinterpret_cast<uint8_t*>(base + o_fl);
   c->d_mask = reinterpret_cast<uint8_t*>(base + o_mask);
   c->d_keys = reinterpret_cast<uint64_t*>(base + o_keys);
+  c->d_counters = reinterpret_cast<int32_t*>(base + o_cnt);
+  c->d_cand_list = reinterpret_cast<int32_t*>(base + o_list);
   c->d_stats = reinterpret_cast<gnmr_stats*>(base + o_st);
 
   if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ptr_stage),
@@ -382,6 +393,9 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   if (e == hipSuccess)
     e = hipMemsetAsync(c->d_Q, 0, size_t(U) * size_t(c->window) * sizeof(double), st);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_lock, 0, size_t(U) * sizeof(int32_t), st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_mask, 0, size_t(U), st);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->d_counters, 0, gnmr::kNumCounters * sizeof(int32_t), st);
   if (e == hipSuccess && S > 0)
     e = hipMemsetAsync(c->d_seg_base, 0, size_t(S) * sizeof(void*), st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);

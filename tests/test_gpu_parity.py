@@ -281,3 +281,47 @@ def test_abi_errors_leave_state_unchanged():
         ctl.step(1.1, 1.5, seg_ptr=[buf.data_ptr()])
         ctl.step(1.1, 1.5)                                   # reuses bound pointers
         assert ctl.query()["stats"]["t"] == 2
+
+
+@pytest.mark.parametrize("case", ["few_ties_at_cut", "many_ties_at_cut", "huge_pool",
+                                  "pool_at_capacity"])
+def test_selection_paths(case):
+    """Top_maxO through each selection path of the kernel: candidates ranked in
+    LDS with index-ordered ties at the cut, more ties than the tie buffer,
+    more candidates than the LDS pool (global keys), and a pool right at it."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller
+
+    rng = np.random.default_rng(11)
+    U, T, max_o, alpha = 3000, 12, 64, 1.1
+    base = np.exp(rng.normal(scale=0.05, size=(T, U)))
+    if case == "few_ties_at_cut":
+        # 300 units share one norm stream and spike together; 20 spike harder
+        tied = rng.choice(U, 300, replace=False)
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+        base[9, tied[:20]] *= 3.0
+        base[9, tied[:20]] += np.arange(20)       # distinct keys above the tie
+    elif case == "many_ties_at_cut":
+        tied = rng.choice(U, 1500, replace=False)
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+    elif case == "huge_pool":
+        U = 10000
+        base = np.exp(rng.normal(scale=0.05, size=(T, U)))
+        alpha = 0.4                                # every unit triggers: |C_t| = U > 4096
+    elif case == "pool_at_capacity":
+        U = 5000
+        base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
+        base[9, :4096] *= 6.0                      # exactly 4096 candidates at t = 10
+    ora = Oracle(U, window=5, max_o=max_o, lock_len=2, eps=1e-12)
+    dn = torch.empty(U, dtype=torch.float64, device="cuda")
+    say("selection path:", case, "units", U)
+    with Controller(U, 5, max_o, 2, 1e-12, np.zeros(U + 1), [], []) as ctl:
+        for t in range(1, T + 1):
+            dn.copy_(torch.from_numpy(base[t - 1]))
+            ctl.step_from_norms(dn, alpha, 1.5)
+            ref = ora.step(base[t - 1], alpha, 1.5)
+            assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} t={t}")
+            if case == "pool_at_capacity" and t == 10:
+                assert ref.stats["n_cand"] == 4096
