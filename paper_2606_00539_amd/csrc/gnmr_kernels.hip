@@ -516,7 +516,7 @@ hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const*
 // would be latency bound.
 static int lanes_per_unit(int64_t num_items, int32_t num_units) {
   const int64_t per = num_items / (num_units > 0 ? num_units : 1);
-  return per < 16 ? 1 : per < 512 ? 64 : 256;
+  return per < 32 ? 1 : per < 512 ? 64 : 256;
 }
 
 template <int L>
