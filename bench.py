@@ -22,6 +22,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# the sources of the gradient-pass kernel whose HBM counters profiles/ records
+K1_SOURCES = ("k1_sumsq.hip", "k1_geometry.h")
 METRIC = "GNMR step GB/s (frac. of HBM peak) + µs/step, 13B-shaped grads, 1 GPU"
 
 
@@ -89,7 +91,7 @@ def measured_traffic(workload: str):
             k, _, v = line.strip().partition("=")
             kv[k] = v
     src = b"".join(open(os.path.join(ROOT, "paper_2606_00539_amd", "csrc", f), "rb").read()
-                   for f in ("gnmr_kernels.hip", "gnmr_internal.h"))
+                   for f in K1_SOURCES)
     if kv.get("kernel_source_sha256_16") != hashlib.sha256(src).hexdigest()[:16]:
         return None
     if kv.get("workload") != workload:

@@ -8,8 +8,10 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libgnmr.so")
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gnmr_runtime.hip", "gnmr_kernels.hip")]
-HEADERS = [os.path.join(PKG, "csrc", "gnmr_internal.h"), os.path.join(ROOT, "include", "gnmr.h")]
+SOURCES = [os.path.join(PKG, "csrc", f)
+           for f in ("gnmr_runtime.hip", "k1_sumsq.hip", "k23_control.hip")]
+HEADERS = [os.path.join(PKG, "csrc", f) for f in ("gnmr_internal.h", "k1_geometry.h")] + [
+    os.path.join(ROOT, "include", "gnmr.h")]
 
 # Packed-fp32 instructions are switched off for all device code.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",
