@@ -50,6 +50,13 @@ typedef enum {
 /* element types of gradient segments */
 enum { GNMR_F32 = 0, GNMR_BF16 = 1 };
 
+/* Budget conventions.  ACTIVE (canonical, Sec. 3.4): maxO caps the active
+ * set, |A_t| <= maxO.  ADMITTED (the budget-convention remark of App. C): maxO
+ * caps only the newly admitted units; candidates already in A_{t-1} stay
+ * active and Top_maxO ranks the remaining candidates, so
+ * A_t = (C_t & A_{t-1}) U Top_maxO(C_t minus A_{t-1}; R). */
+enum { GNMR_BUDGET_ACTIVE = 0, GNMR_BUDGET_ADMITTED = 1 };
+
 /* Controller settings (Alg. 1 and Alg. 2 inputs that do not change per step). */
 typedef struct {
   int32_t num_units;          /* |B| >= 1, monitored units                       */
@@ -58,6 +65,11 @@ typedef struct {
   int32_t lock_len;           /* T_lock >= 0                                      */
   double eps;                 /* epsilon >= 0, finite                              */
   const uint8_t* recoverable; /* host [num_units], nonzero = in B_rec; NULL = all */
+  int32_t budget_mode;        /* GNMR_BUDGET_ACTIVE or GNMR_BUDGET_ADMITTED        */
+  int32_t warmup_steps;       /* W >= 0: for t <= W every recoverable unit takes the
+                                 recovery path (high-fidelity warm-up, App. E.6):
+                                 C_t = A_t = B_rec, the lock rule of Alg. 2 applies,
+                                 GNMR state updates as usual; 0 = none           */
 } gnmr_config;
 
 /* Gradient layout: unit b owns segments [unit_seg_off[b], unit_seg_off[b+1]).
@@ -85,8 +97,10 @@ typedef struct {
   int32_t n_trig_dgnmr;  /* #{Delta-GNMR/beta_t > 1}                               */
   int32_t n_trig;        /* #{R > 1}                                               */
   int32_t n_cand;        /* |C_t|                                                  */
-  int32_t n_active;      /* |A_t| <= maxO                                          */
-  int32_t hit_maxo;      /* 1 if C_t is non-empty and |C_t| >= maxO                */
+  int32_t n_active;      /* |A_t| (<= maxO under GNMR_BUDGET_ACTIVE)               */
+  int32_t hit_maxo;      /* 1 if the ranked pool (C_t, or C_t minus A_{t-1} under
+                            GNMR_BUDGET_ADMITTED) is non-empty and >= maxO; 0 in
+                            the warm-up                                           */
   int32_t n_nonfinite;   /* units with a non-finite norm                           */
   int32_t reserved;
 } gnmr_stats;
@@ -139,7 +153,7 @@ gnmr_status gnmr_device_outputs(gnmr_ctx* ctx, const uint8_t** mask,
                                 const double** gnmr, const double** dgnmr,
                                 const double** risk, const gnmr_stats** stats);
 
-/* Controller state (t, A, Q, Lock) as a flat, versioned byte blob, for
+/* Controller state (t, A, Q, Lock, A_{t-1}) as a flat, versioned byte blob, for
  * checkpoint and resume.  gnmr_state_size gives the blob size; get copies it
  * to host `buf` of `bytes` >= that size (waits for `stream`); set restores a
  * blob taken from a context with the same num_units and window.  Restoring and

@@ -37,7 +37,16 @@ Readings where the paper is silent (each also listed in the design doc):
     1.0 pushed into Q_b, counted in n_nonfinite.
   * Statistics: n_trig_gnmr = #{GNMR/alpha > 1}, n_trig_dgnmr =
     #{D-GNMR/beta > 1}, n_trig = #{R > 1}, all over recoverable units;
-    hit_maxo = 1 when |C_t| >= maxO and C_t is non-empty.
+    hit_maxo = 1 when the ranked pool is non-empty and at least maxO large.
+
+Policy variants (both off by default):
+  * budget_mode = BUDGET_ADMITTED caps only the newly admitted units, as the
+    budget-convention remark of App. C allows: the candidates already in
+    A_{t-1} stay active, and Top_maxO ranks the other candidates
+    (A_t = (C_t & A_{t-1}) U Top_maxO(C_t minus A_{t-1}; R)).
+  * warmup_steps = W: for t <= W every recoverable unit takes the recovery
+    path (the high-fidelity warm-up of App. E.6): C_t = A_t = B_rec and the
+    lock rule of Alg. 2 is applied to it; GNMR state updates as usual.
 """
 from __future__ import annotations
 
@@ -48,6 +57,10 @@ import numpy as np
 
 F32 = 0
 BF16 = 1
+
+# budget conventions (Sec. 3.4; the budget-convention remark of App. C)
+BUDGET_ACTIVE = 0      # |A_t| <= maxO (canonical)
+BUDGET_ADMITTED = 1    # |A_t minus A_{t-1}| <= maxO: only newly admitted units count
 
 
 # --------------------------------------------------------------------------
@@ -103,9 +116,12 @@ class Controller:
     GNMR queues Q_b (length <= delta), lock counters Lock_b."""
 
     def __init__(self, num_units: int, window: int, max_o: int, lock_len: int,
-                 eps: float, recoverable=None):
+                 eps: float, recoverable=None, budget_mode: int = BUDGET_ACTIVE,
+                 warmup_steps: int = 0):
         if num_units < 1 or window < 1 or max_o < 0 or lock_len < 0:
             raise ValueError("need num_units >= 1, window >= 1, max_o >= 0, lock_len >= 0")
+        if budget_mode not in (BUDGET_ACTIVE, BUDGET_ADMITTED) or warmup_steps < 0:
+            raise ValueError("unknown budget_mode or negative warmup_steps")
         if not (eps >= 0.0 and math.isfinite(eps)):
             raise ValueError("need finite eps >= 0")
         self.U = int(num_units)
@@ -119,21 +135,25 @@ class Controller:
             self.rec = np.asarray(recoverable).astype(bool).reshape(-1)
             if self.rec.size != self.U:
                 raise ValueError("recoverable must have num_units entries")
+        self.budget_mode = int(budget_mode)
+        self.warmup_steps = int(warmup_steps)
         self.t = 0                                   # steps taken so far
         self.A = np.zeros(self.U)                    # historical means A_b
         self.Q: list[np.ndarray] = []                # oldest first, each [U]
         self.lock = np.zeros(self.U, dtype=np.int64)
+        self.active = np.zeros(self.U, dtype=bool)   # A_{t-1}
 
     # -- state snapshot -----------------------------------------------------
     def get_state(self) -> dict:
         return {"t": self.t, "A": self.A.copy(), "Q": [q.copy() for q in self.Q],
-                "lock": self.lock.copy()}
+                "lock": self.lock.copy(), "active": self.active.copy()}
 
     def set_state(self, st: dict) -> None:
         self.t = int(st["t"])
         self.A = np.array(st["A"], dtype=np.float64)
         self.Q = [np.array(q, dtype=np.float64) for q in st["Q"]]
         self.lock = np.array(st["lock"], dtype=np.int64)
+        self.active = np.array(st["active"], dtype=bool)
 
     # -- one controller step --------------------------------------------------
     def step(self, norms, alpha: float, beta: float) -> StepResult:
@@ -181,14 +201,29 @@ class Controller:
         # Alg. 2: candidate pool (lock counters from the previous step).
         triggered = self.rec & (risk > 1.0)
         cand = triggered | (self.rec & (self.lock > 0))
+        warm = t <= self.warmup_steps
+        if warm:
+            # high-fidelity warm-up (App. E.6): every recoverable unit recovers
+            cand = self.rec.copy()
         cand_idx = np.flatnonzero(cand)
 
-        # Alg. 2: Top_maxO by R, ties to the smaller index.
-        if cand_idx.size <= self.max_o:
-            active = cand_idx
+        # Units that skip the ranking: all of them during the warm-up; under the
+        # admitted-only budget, the candidates already active at t-1.
+        if warm:
+            keep = cand
+        elif self.budget_mode == BUDGET_ADMITTED:
+            keep = cand & self.active
         else:
-            order = np.lexsort((cand_idx, -risk[cand_idx]))
-            active = cand_idx[order[: self.max_o]]
+            keep = np.zeros(U, dtype=bool)
+        pool_idx = np.flatnonzero(cand & ~keep)
+
+        # Alg. 2: Top_maxO by R, ties to the smaller index.
+        if pool_idx.size <= self.max_o:
+            admitted = pool_idx
+        else:
+            order = np.lexsort((pool_idx, -risk[pool_idx]))
+            admitted = pool_idx[order[: self.max_o]]
+        active = np.union1d(np.flatnonzero(keep), admitted).astype(np.int64)
         mask = np.zeros(U, dtype=np.uint8)
         mask[active] = 1
 
@@ -200,6 +235,7 @@ class Controller:
             else:
                 new_lock[b] = max(self.lock[b] - 1, 0)
         self.lock = new_lock
+        self.active = mask.astype(bool)
         self.t = t
 
         stats = {
@@ -209,7 +245,7 @@ class Controller:
             "n_trig": int(np.count_nonzero(triggered)),
             "n_cand": int(cand_idx.size),
             "n_active": int(active.size),
-            "hit_maxo": int(cand_idx.size > 0 and cand_idx.size >= self.max_o),
+            "hit_maxo": int(not warm and pool_idx.size > 0 and pool_idx.size >= self.max_o),
             "n_nonfinite": int(np.count_nonzero(~finite)),
         }
         return StepResult(t, n.copy(), gnmr, dgnmr, risk, mask,

@@ -17,6 +17,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgnmr.so
 
 GNMR_OK, GNMR_E_INVALID, GNMR_E_NOMEM, GNMR_E_HIP, GNMR_E_STATE = 0, -1, -2, -3, -4
 GNMR_F32, GNMR_BF16 = 0, 1
+GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED = 0, 1
 STATUS_NAMES = {0: "GNMR_OK", -1: "GNMR_E_INVALID", -2: "GNMR_E_NOMEM", -3: "GNMR_E_HIP",
                 -4: "GNMR_E_STATE"}
 
@@ -35,7 +36,8 @@ class GnmrError(RuntimeError):
 class gnmr_config(ctypes.Structure):
     _fields_ = [("num_units", ctypes.c_int32), ("window", ctypes.c_int32),
                 ("max_o", ctypes.c_int32), ("lock_len", ctypes.c_int32),
-                ("eps", ctypes.c_double), ("recoverable", ctypes.c_void_p)]
+                ("eps", ctypes.c_double), ("recoverable", ctypes.c_void_p),
+                ("budget_mode", ctypes.c_int32), ("warmup_steps", ctypes.c_int32)]
 
 
 class gnmr_segments(ctypes.Structure):
@@ -113,14 +115,16 @@ def _stream(stream) -> int:
 # -- one Python function per C entry point ------------------------------------
 
 def gnmr_init(num_units, window, max_o, lock_len, eps, unit_seg_off, seg_numel, seg_dtype,
-              seg_ptr=None, recoverable=None, stream=None) -> ctypes.c_void_p:
+              seg_ptr=None, recoverable=None, stream=None, budget_mode=GNMR_BUDGET_ACTIVE,
+              warmup_steps=0) -> ctypes.c_void_p:
     lib = load_library()
     uso = np.ascontiguousarray(unit_seg_off, dtype=np.int64)
     numel = np.ascontiguousarray(seg_numel, dtype=np.int64)
     dt = np.ascontiguousarray(seg_dtype, dtype=np.int32)
     rec = None if recoverable is None else np.ascontiguousarray(recoverable, dtype=np.uint8)
     cfg = gnmr_config(int(num_units), int(window), int(max_o), int(lock_len), float(eps),
-                      None if rec is None else rec.ctypes.data)
+                      None if rec is None else rec.ctypes.data, int(budget_mode),
+                      int(warmup_steps))
     ptrs = None if seg_ptr is None else _ptr_array(seg_ptr)
     segs = gnmr_segments(int(numel.size), uso.ctypes.data, numel.ctypes.data, dt.ctypes.data,
                          None if ptrs is None else ctypes.cast(ptrs, ctypes.c_void_p))
@@ -222,10 +226,11 @@ class Controller:
     """One GNMR controller context over a fixed segment layout."""
 
     def __init__(self, num_units, window, max_o, lock_len, eps, unit_seg_off, seg_numel,
-                 seg_dtype, seg_ptr=None, recoverable=None, stream=None):
+                 seg_dtype, seg_ptr=None, recoverable=None, stream=None,
+                 budget_mode=GNMR_BUDGET_ACTIVE, warmup_steps=0):
         self.num_units = int(num_units)
         self.ctx = gnmr_init(num_units, window, max_o, lock_len, eps, unit_seg_off, seg_numel,
-                             seg_dtype, seg_ptr, recoverable, stream)
+                             seg_dtype, seg_ptr, recoverable, stream, budget_mode, warmup_steps)
 
     def step(self, alpha_t, beta_t, seg_ptr=None, stream=None):
         gnmr_step(self.ctx, alpha_t, beta_t, seg_ptr, stream)

@@ -16,6 +16,7 @@ enum : int {
   kCntTrigD = 2,      // recoverable units with Delta-GNMR / beta > 1
   kCntTrigR = 3,      // recoverable units with R > 1
   kCntNonFinite = 4,  // units with a non-finite norm
+  kCntRank = 5,       // members of C_t that are ranked for the budget
   kNumCounters = 8
 };
 
@@ -26,7 +27,9 @@ enum : uint8_t {
   kFlagNonFinite = 4,  // non-finite norm
   kFlagTrigR = 8,      // R > 1
   kFlagRec = 16,       // recoverable
-  kFlagCand = 32       // member of the candidate pool C_t
+  kFlagCand = 32,      // member of the candidate pool C_t
+  kFlagKeep = 64       // active without ranking (warm-up; continuing unit under
+                       // the admitted-only budget)
 };
 
 struct UpdateArgs {
@@ -35,6 +38,8 @@ struct UpdateArgs {
   int32_t qlen;        // values in Q before this step (min(t-1, delta))
   int32_t slot;        // ring slot of the oldest value == slot of the new value
   int64_t t;           // this step, 1-based
+  int32_t warm;        // t <= warmup_steps
+  int32_t admitted;    // budget_mode == GNMR_BUDGET_ADMITTED
   double eps, alpha, beta;
   const int64_t* unit_item_off;  // [U+1]
   const float* partial;          // [items]
@@ -49,7 +54,7 @@ struct UpdateArgs {
   int32_t* lock;                 // [U], Lock after step t-1 (cleared for units outside C_t)
   uint64_t* keys;                // [U], candidate key or 0
   uint8_t* flags;
-  uint8_t* mask;                 // [U], cleared for units outside C_t
+  uint8_t* mask;                 // [U], A_{t-1} on entry; cleared for units outside C_t
   int32_t* counters;             // [kNumCounters], zero on entry
   int32_t* cand_list;            // [U], members of C_t (any order), counters[kCntCand] of them
 };
@@ -58,6 +63,7 @@ struct SelectArgs {
   int32_t num_units;
   int32_t max_o;
   int32_t lock_len;
+  int32_t warm;
   int64_t t;
   const uint8_t* flags;
   const uint64_t* keys;

@@ -30,7 +30,7 @@ gnmr_status fail(gnmr_status st, const std::string& msg) {
   } while (0)
 
 constexpr uint32_t kStateMagic = 0x524D4E47u;  // "GNMR"
-constexpr uint32_t kStateVersion = 1;
+constexpr uint32_t kStateVersion = 2;
 constexpr int kProfileCapacity = 4096;
 
 struct StateHeader {
@@ -69,6 +69,7 @@ struct DeviceGuard {
 struct gnmr_ctx {
   int device = 0;
   int32_t U = 0, window = 0, max_o = 0, lock_len = 0;
+  int32_t budget_mode = GNMR_BUDGET_ACTIVE, warmup_steps = 0;
   double eps = 0.0;
   int64_t S = 0;
   std::vector<int64_t> seg_numel;
@@ -174,6 +175,8 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   u.qlen = int32_t(std::min<int64_t>(t - 1, c->window));
   u.slot = int32_t((t - 1) % c->window);
   u.t = t;
+  u.warm = t <= c->warmup_steps ? 1 : 0;
+  u.admitted = c->budget_mode == GNMR_BUDGET_ADMITTED ? 1 : 0;
   u.eps = c->eps;
   u.alpha = alpha;
   u.beta = beta;
@@ -201,6 +204,7 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   s.num_units = c->U;
   s.max_o = c->max_o;
   s.lock_len = c->lock_len;
+  s.warm = u.warm;
   s.t = t;
   s.flags = c->d_flags;
   s.keys = c->d_keys;
@@ -249,6 +253,9 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   if (cfg->lock_len < 0) return fail(GNMR_E_INVALID, "lock_len must be >= 0");
   if (!(cfg->eps >= 0.0) || !isfinite(cfg->eps))
     return fail(GNMR_E_INVALID, "eps must be finite and >= 0");
+  if (cfg->budget_mode != GNMR_BUDGET_ACTIVE && cfg->budget_mode != GNMR_BUDGET_ADMITTED)
+    return fail(GNMR_E_INVALID, "unknown budget_mode " + std::to_string(cfg->budget_mode));
+  if (cfg->warmup_steps < 0) return fail(GNMR_E_INVALID, "warmup_steps must be >= 0");
   const int64_t U = cfg->num_units, S = segs->num_segments;
   if (S < 0 || S > INT32_MAX) return fail(GNMR_E_INVALID, "num_segments out of range");
   if (segs->unit_seg_off == nullptr) return fail(GNMR_E_INVALID, "unit_seg_off is NULL");
@@ -271,6 +278,8 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   c->window = cfg->window;
   c->max_o = cfg->max_o;
   c->lock_len = cfg->lock_len;
+  c->budget_mode = cfg->budget_mode;
+  c->warmup_steps = cfg->warmup_steps;
   c->eps = cfg->eps;
   c->S = S;
   c->seg_numel.assign(segs->seg_numel, segs->seg_numel + S);
@@ -512,7 +521,7 @@ gnmr_status gnmr_state_size(const gnmr_ctx* ctx, size_t* bytes) {
   if (ctx == nullptr || bytes == nullptr) return fail(GNMR_E_INVALID, "NULL argument");
   const size_t U = size_t(ctx->U);
   *bytes = sizeof(StateHeader) + U * sizeof(double) * (1 + size_t(ctx->window)) +
-           U * sizeof(int32_t);
+           U * sizeof(int32_t) + U;
   return GNMR_OK;
 }
 
@@ -536,6 +545,8 @@ gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream)
                           hipMemcpyDeviceToHost, st));
   p += U * size_t(ctx->window) * sizeof(double);
   GNMR_HIP(hipMemcpyAsync(p, ctx->d_lock, U * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  p += U * sizeof(int32_t);
+  GNMR_HIP(hipMemcpyAsync(p, ctx->d_mask, U, hipMemcpyDeviceToHost, st));
   GNMR_HIP(hipStreamSynchronize(st));
   return GNMR_OK;
 }
@@ -563,6 +574,8 @@ gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* s
                           hipMemcpyHostToDevice, st));
   p += U * size_t(ctx->window) * sizeof(double);
   GNMR_HIP(hipMemcpyAsync(ctx->d_lock, p, U * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  p += U * sizeof(int32_t);
+  GNMR_HIP(hipMemcpyAsync(ctx->d_mask, p, U, hipMemcpyHostToDevice, st));
   GNMR_HIP(hipStreamSynchronize(st));
   ctx->t = h.t;
   return GNMR_OK;

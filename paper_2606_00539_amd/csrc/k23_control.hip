@@ -120,16 +120,25 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   const double R = gt > dt ? gt : dt;
   const bool rec = a.rec[b] != 0;
   const bool trig = R > 1.0;
-  const bool cand = rec && (trig || a.lock[b] > 0);
+  bool cand = rec && (trig || a.lock[b] > 0);
+  bool keep = false;
+  if (a.warm) {                       // warm-up: C_t = A_t = B_rec
+    cand = rec;
+    keep = rec;
+  } else if (a.admitted && cand) {    // admitted-only budget: A_{t-1} members stay
+    keep = a.mask[b] != 0;
+  }
+  const bool ranked = cand && !keep;
   const bool tg = rec && gt > 1.0, td = rec && dt > 1.0, tr = rec && trig;
   a.norm[b] = n;
   a.gnmr[b] = G;
   a.dgnmr[b] = D;
   a.risk[b] = R;
-  a.keys[b] = cand ? cand_key(R) : 0;
+  a.keys[b] = ranked ? cand_key(R) : 0;
   a.flags[b] = uint8_t((gt > 1.0 ? kFlagTrigG : 0) | (dt > 1.0 ? kFlagTrigD : 0) |
                        (finite ? 0 : kFlagNonFinite) | (trig ? kFlagTrigR : 0) |
-                       (rec ? kFlagRec : 0) | (cand ? kFlagCand : 0));
+                       (rec ? kFlagRec : 0) | (cand ? kFlagCand : 0) |
+                       (keep ? kFlagKeep : 0));
   // Alg. 2 outcome of a unit outside C_t is fixed already: low-cost path,
   // Lock = 0.  K3 only has to rank and update the members of C_t.
   if (!cand) {
@@ -144,10 +153,11 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
     const int wl = threadIdx.x & 63;
     const uint64_t m_c = __ballot(cand);
     const uint64_t m_g = __ballot(tg), m_d = __ballot(td), m_r = __ballot(tr);
-    const uint64_t m_n = __ballot(!finite);
+    const uint64_t m_n = __ballot(!finite), m_k = __ballot(ranked);
     int base = 0;
     if (wl == leader) {
       if (m_c) base = atomicAdd(&a.counters[kCntCand], __popcll(m_c));
+      if (m_k) atomicAdd(&a.counters[kCntRank], __popcll(m_k));
       if (m_g) atomicAdd(&a.counters[kCntTrigG], __popcll(m_g));
       if (m_d) atomicAdd(&a.counters[kCntTrigD], __popcll(m_d));
       if (m_r) atomicAdd(&a.counters[kCntTrigR], __popcll(m_r));
@@ -157,6 +167,7 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
     if (cand) a.cand_list[base + __popcll(m_c & ((uint64_t(1) << wl) - 1))] = b;
   } else {
     if (cand) a.cand_list[atomicAdd(&a.counters[kCntCand], 1)] = b;
+    if (ranked) atomicAdd(&a.counters[kCntRank], 1);
     if (tg) atomicAdd(&a.counters[kCntTrigG], 1);
     if (td) atomicAdd(&a.counters[kCntTrigD], 1);
     if (tr) atomicAdd(&a.counters[kCntTrigR], 1);
@@ -215,9 +226,9 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
   return prefix;
 }
 
-// Selection over every unit from the global keys: key > T, or key == T and
-// among the first `need` such units in index order (contiguous index ranges
-// per thread and an exclusive scan of their tie counts).
+// Selection over every unit from the global keys: kept units, key > T, or
+// key == T and among the first `need` such units in index order (contiguous
+// index ranges per thread and an exclusive scan of their tie counts).
 __device__ int select_by_scan(const SelectArgs& a, uint64_t T, int need, uint32_t* scan) {
   const int tid = threadIdx.x;
   const int U = a.num_units;
@@ -238,12 +249,14 @@ __device__ int select_by_scan(const SelectArgs& a, uint64_t T, int need, uint32_
   int c_act = 0;
   for (int b = lo; b < hi; ++b) {
     const uint64_t key = a.keys[b];
+    const uint8_t f = a.flags[b];
     bool sel = key > T;
     if (key == T) {
       sel = rank < uint32_t(need);
       ++rank;
     }
-    apply_selection(a, b, sel, a.flags[b]);
+    sel = sel || (f & kFlagKeep);
+    apply_selection(a, b, sel, f);
     c_act += sel;
   }
   return c_act;
@@ -269,12 +282,14 @@ __device__ void bitonic_sort(int32_t* v) {
   __syncthreads();
 }
 
-// K3: a single workgroup, over the members of C_t listed by K2.  When
-// |C_t| <= maxO every candidate is active.  Otherwise Top_maxO needs the
-// maxO-th largest key T (radix select): every candidate with key > T is
-// active, and the first `need` candidates with key == T in index order.
-// Pools of up to kK3Cap candidates are ranked in LDS; larger ones over the
-// global keys of all units.
+// K3: a single workgroup, over the members of C_t listed by K2.  Kept units
+// (warm-up; continuing units under the admitted-only budget) are active
+// without ranking; the others are ranked for the budget.  When at most maxO
+// are ranked they are all active.  Otherwise Top_maxO needs the maxO-th
+// largest ranked key T (radix select; kept units carry key 0): every ranked
+// candidate with key > T is active, and the first `need` with key == T in
+// index order.  Pools of up to kK3Cap candidates are ranked in LDS; larger
+// ones over the global keys of all units.
 __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
   __shared__ uint64_t c_key[kK3Cap];
   __shared__ int32_t c_idx[kK3Cap];
@@ -286,17 +301,20 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
   const int tid = threadIdx.x;
   const int U = a.num_units;
   const int n_cand = a.counters[kCntCand];
+  const int n_rank = a.counters[kCntRank];
   if (tid < 2) cnt[tid] = 0;
   __syncthreads();
 
   int c_act = 0;
-  if (a.max_o == 0 || n_cand <= a.max_o) {
-    // A_t = C_t (or empty when maxO = 0): no ranking needed.
+  if (a.max_o == 0 || n_rank <= a.max_o) {
+    // no ranking: every listed unit is active, or only the kept ones if maxO = 0
     const bool take = a.max_o > 0;
     for (int i = tid; i < n_cand; i += kK3Block) {
       const int b = a.cand_list[i];
-      apply_selection(a, b, take, a.flags[b]);
-      c_act += take;
+      const uint8_t f = a.flags[b];
+      const bool sel = take || (f & kFlagKeep);
+      apply_selection(a, b, sel, f);
+      c_act += sel;
     }
   } else if (n_cand > kK3Cap) {
     int need = 0;
@@ -336,8 +354,9 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
       for (int i = tid; i < n_cand; i += kK3Block) {
         const int b = c_idx[i];
         const uint64_t key = c_key[i];
-        const bool sel = key > T || (key == T && b <= cut);
-        apply_selection(a, b, sel, a.flags[b]);
+        const uint8_t f = a.flags[b];
+        const bool sel = key > T || (key == T && b <= cut) || (f & kFlagKeep);
+        apply_selection(a, b, sel, f);
         c_act += sel;
       }
     }
@@ -352,7 +371,7 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
     st.n_trig = a.counters[kCntTrigR];
     st.n_cand = n_cand;
     st.n_active = cnt[0];
-    st.hit_maxo = (n_cand > 0 && n_cand >= a.max_o) ? 1 : 0;
+    st.hit_maxo = (!a.warm && n_rank > 0 && n_rank >= a.max_o) ? 1 : 0;
     st.n_nonfinite = a.counters[kCntNonFinite];
     st.reserved = 0;
     *a.stats = st;

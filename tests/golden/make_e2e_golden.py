@@ -14,10 +14,14 @@ Stored per workload:
   lock         uint8 [T, U] lock counters after each step
   stats        int64 [T, 8] counters (t, n_trig_gnmr, n_trig_dgnmr, n_trig,
                n_cand, n_active, hit_maxo, n_nonfinite)
-  norm32       float32 [T, U] oracle norms (float32 is far inside the 1e-5 bar)
+  norm32       float32 [len(norm_steps), U] oracle norms (float32 is far inside
+               the 1e-5 bar) at the 1-based steps norm_steps: every step, or for
+               workloads of more than 400k unit-steps steps 1, 2 and every 16th
   sample       int64 [S] unit indices with float64 gnmr/dgnmr/risk [T, S]
 
 Usage: python tests/golden/make_e2e_golden.py [workload ...] [--threads N]
+       python tests/golden/make_e2e_golden.py --thin workload ...   (rewrite an
+       existing file with the norm subsampling above)
 """
 from __future__ import annotations
 
@@ -41,12 +45,34 @@ from synth import host  # noqa: E402
 from synth import recipe as R  # noqa: E402
 
 CHUNK = 1 << 22
+FULL_NORMS_MAX = 400_000      # unit-steps up to which every step's norms are kept
 STAT_KEYS = ("t", "n_trig_gnmr", "n_trig_dgnmr", "n_trig", "n_cand", "n_active", "hit_maxo",
              "n_nonfinite")
 
 
 def golden_path(name: str) -> str:
     return os.path.join(HERE, f"e2e_{name}.npz")
+
+
+def norm_steps_for(steps: int, units: int) -> np.ndarray:
+    if steps * units <= FULL_NORMS_MAX:
+        return np.arange(1, steps + 1, dtype=np.int64)
+    return np.array([t for t in range(1, steps + 1) if t <= 2 or t % 16 == 0], dtype=np.int64)
+
+
+def thin(name: str) -> str:
+    """Rewrite a golden file keeping norms only at norm_steps_for(...)."""
+    path = golden_path(name)
+    z = np.load(path, allow_pickle=False)
+    d = {k: z[k] for k in z.files}
+    T, U = int(d["steps"]), int(d["units"])
+    keep = norm_steps_for(T, U)
+    old = d.get("norm_steps", np.arange(1, T + 1, dtype=np.int64))
+    rows = [int(np.flatnonzero(old == t)[0]) for t in keep]
+    d["norm32"] = d["norm32"][rows]
+    d["norm_steps"] = keep
+    np.savez_compressed(path, **d)
+    return path
 
 
 def unit_norm(seed, t, b, scale32, dtype, numel):
@@ -92,7 +118,8 @@ def make(name: str, threads: int) -> str:
         nudge_t=(nt + 1).astype(np.int64), nudge_b=nb.astype(np.int64),
         nudge_f=nudge[nt, nb],
         mask_bits=np.packbits(masks, axis=1), lock=locks.astype(np.uint8), stats=stats,
-        norm32=norms.astype(np.float32), sample=sample,
+        norm_steps=norm_steps_for(T, U),
+        norm32=norms[norm_steps_for(T, U) - 1].astype(np.float32), sample=sample,
         gnmr=np.stack([r.gnmr[sample] for r in res]),
         dgnmr=np.stack([r.dgnmr[sample] for r in res]),
         risk=np.stack([r.risk[sample] for r in res]))
@@ -106,6 +133,8 @@ def load(name: str) -> dict:
     z = np.load(golden_path(name), allow_pickle=False)
     d = {k: z[k] for k in z.files}
     d["mask"] = np.unpackbits(d["mask_bits"], axis=1, count=int(d["units"])).astype(np.uint8)
+    if "norm_steps" not in d:
+        d["norm_steps"] = np.arange(1, int(d["steps"]) + 1, dtype=np.int64)
     return d
 
 
@@ -120,6 +149,7 @@ if __name__ == "__main__":
     ap.add_argument("workloads", nargs="*",
                     default=["tiny", "llama2-7b", "llama2-13b", "moe", "fine128", "fine32"])
     ap.add_argument("--threads", type=int, default=os.cpu_count() or 8)
+    ap.add_argument("--thin", action="store_true")
     a = ap.parse_args()
     for n in a.workloads:
-        make(n, a.threads)
+        print(thin(n) if a.thin else make(n, a.threads), flush=True)

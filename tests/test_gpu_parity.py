@@ -325,3 +325,55 @@ def test_selection_paths(case):
             assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} t={t}")
             if case == "pool_at_capacity" and t == 10:
                 assert ref.stats["n_cand"] == 4096
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama2-13b", "moe", "fine32"])
+@pytest.mark.parametrize("policy", ["admitted", "warmup", "admitted_warmup", "admitted_alpha04"])
+def test_policy_variants(name, policy):
+    """The admitted-only budget (App. C budget-convention remark) and the
+    high-fidelity warm-up (App. E.6) against the oracle, norm-level streams."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED, Controller
+
+    w = R.get(name)
+    norms = R.surrogate_norms(w, seed=3)
+    mode = GNMR_BUDGET_ADMITTED if policy.startswith("admitted") else GNMR_BUDGET_ACTIVE
+    warm = int(np.ceil(0.05 * w.steps)) if "warmup" in policy else 0
+    alpha_of = (lambda t: 0.4) if policy.endswith("alpha04") else w.alpha
+    say("policy:", name, policy, "warm-up", warm)
+    ora = Oracle(w.num_units, window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=w.eps,
+                 budget_mode=mode, warmup_steps=warm)
+    dn = torch.empty(w.num_units, dtype=torch.float64, device="cuda")
+    with Controller(w.num_units, w.window, w.max_o, w.lock_len, w.eps, np.zeros(w.num_units + 1),
+                    [], [], budget_mode=mode, warmup_steps=warm) as ctl:
+        for t in range(1, w.steps + 1):
+            dn.copy_(torch.from_numpy(norms[t - 1]))
+            ctl.step_from_norms(dn, alpha_of(t), w.beta(t))
+            ref = ora.step(norms[t - 1], alpha_of(t), w.beta(t))
+            assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{name}/{policy} t={t}")
+
+
+def test_state_roundtrip_admitted_keeps_previous_active_set():
+    torch = require_gpu()
+    from paper_2606_00539_amd import GNMR_BUDGET_ADMITTED, Controller
+
+    w = R.get("fine128")
+    norms = R.surrogate_norms(w)[:40]
+    dn = torch.empty(w.num_units, dtype=torch.float64, device="cuda")
+    mk = lambda: Controller(w.num_units, w.window, w.max_o, w.lock_len, w.eps,
+                            np.zeros(w.num_units + 1), [], [], budget_mode=GNMR_BUDGET_ADMITTED)
+    a, b = mk(), mk()
+    for t in range(1, 21):
+        dn.copy_(torch.from_numpy(norms[t - 1]))
+        a.step_from_norms(dn, 0.9, 1.5)
+    b.set_state(a.get_state())
+    for t in range(21, 41):
+        dn.copy_(torch.from_numpy(norms[t - 1]))
+        a.step_from_norms(dn, 0.9, 1.5)
+        b.step_from_norms(dn, 0.9, 1.5)
+        qa, qb = a.query(), b.query()
+        for f in ("mask", "lock", "norm", "gnmr", "dgnmr", "risk"):
+            assert np.array_equal(qa[f], qb[f])
+        assert qa["stats"] == qb["stats"]
+    a.close()
+    b.close()

@@ -30,18 +30,20 @@ MUTANTS = [
      "cand = triggered"),
     ("non-recoverable selectable", "triggered = self.rec & (risk > 1.0)",
      "triggered = (risk > 1.0)"),
-    ("ascending selection", "order = np.lexsort((cand_idx, -risk[cand_idx]))",
-     "order = np.lexsort((cand_idx, risk[cand_idx]))"),
-    ("ties to larger index", "order = np.lexsort((cand_idx, -risk[cand_idx]))",
-     "order = np.lexsort((-cand_idx, -risk[cand_idx]))"),
+    ("ascending selection", "order = np.lexsort((pool_idx, -risk[pool_idx]))",
+     "order = np.lexsort((pool_idx, risk[pool_idx]))"),
+    ("ties to larger index", "order = np.lexsort((pool_idx, -risk[pool_idx]))",
+     "order = np.lexsort((-pool_idx, -risk[pool_idx]))"),
     ("lock set to T_lock - 1", "new_lock[b] = self.lock_len", "new_lock[b] = self.lock_len - 1"),
     ("lock not decremented", "new_lock[b] = max(self.lock[b] - 1, 0)",
      "new_lock[b] = max(self.lock[b], 0)"),
     ("eviction keeps lock", "new_lock = np.zeros(U, dtype=np.int64)", "new_lock = self.lock.copy()"),
-    ("budget off by one", "if cand_idx.size <= self.max_o:", "if cand_idx.size <= self.max_o + 1:"),
+    ("budget off by one", "if pool_idx.size <= self.max_o:", "if pool_idx.size <= self.max_o + 1:"),
     ("L1 instead of L2", "s += float(np.dot(x, x))", "s += float(np.sum(np.abs(x)))"),
     ("bf16 widened wrongly", "<< np.uint32(16)", "<< np.uint32(15)"),
     ("GNMR not clamped at A = 0", "has_mean = finite & (self.A != 0.0)", "has_mean = finite"),
+    ("admitted mode keeps every candidate", "keep = cand & self.active", "keep = cand"),
+    ("warm-up ignored", "cand = self.rec.copy()", "cand = cand"),
     ("current GNMR in window", "for q in self.Q:                       # oldest to newest",
      "for q in self.Q[1:] + [gnmr]:"),
 ]
@@ -62,6 +64,8 @@ PINS = [
     (P.test_non_recoverable_units_are_monitored_only, {}),
     (P.test_eps_enters_both_denominators, {}),
     (P.test_trigger_is_strict, {}),
+    (P.test_admitted_only_budget_brute_force, dict(seed=0)),
+    (P.test_warmup_all_recover_then_normal, dict(max_o=3)),
 ]
 
 

@@ -403,3 +403,80 @@ def test_trigger_is_strict():
     for t in range(10):
         r = ctl.step([0.25, 4.0], 1.0, 1.0)
         assert np.all(r.risk == 1.0) and r.mask.sum() == 0 and r.stats["n_trig"] == 0
+
+
+# --------------------------------------------------------------------------
+# policy variants: admitted-only budget (App. C remark), warm-up (App. E.6)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(4))
+def test_admitted_only_budget_brute_force(seed):
+    from oracle import BUDGET_ADMITTED
+
+    rng = np.random.default_rng(200 + seed)
+    U, max_o, lock_len, T = 9, 2, 3, 40
+    norms = np.exp(rng.normal(scale=0.5, size=(T, U)))
+    ctl = Controller(U, window=3, max_o=max_o, lock_len=lock_len, eps=0.0,
+                     budget_mode=BUDGET_ADMITTED)
+    prev_active = np.zeros(U, bool)
+    lock_before = np.zeros(U, np.int64)
+    grew = False
+    for t in range(1, T + 1):
+        r = ctl.step(norms[t - 1], 1.05, 1.1)
+        cand = (r.risk > 1.0) | (lock_before > 0)
+        A = r.mask.astype(bool)
+        keep = cand & prev_active
+        assert np.array_equal(A & prev_active, keep)           # continuing units retained
+        assert not np.any(A & ~cand)                            # A_t within C_t
+        new = A & ~prev_active
+        assert new.sum() <= max_o                               # cap on admissions only
+        pool = cand & ~prev_active
+        assert set(np.flatnonzero(new)) == brute_force_active(r.risk, pool, max_o)
+        grew |= A.sum() > max_o
+        prev_active, lock_before = A, r.lock.astype(np.int64)
+    assert grew                    # the active set itself may exceed maxO in this mode
+
+
+def test_admitted_only_equals_active_cap_when_nothing_was_active():
+    from oracle import BUDGET_ADMITTED
+
+    rng = np.random.default_rng(9)
+    U = 30
+    norms = np.exp(rng.normal(scale=0.5, size=(2, U)))
+    # alpha = 0.05: every unit triggers at t = 1 and 2; lock 0.  At t = 1
+    # (A_0 empty) the two conventions agree; at t = 2 the admitted-only budget
+    # keeps the 4 active units and admits 4 more.
+    a = Controller(U, 5, 4, 0, 0.0)
+    b = Controller(U, 5, 4, 0, 0.0, budget_mode=BUDGET_ADMITTED)
+    ra, rb = a.step(norms[0], 0.05, 1.5), b.step(norms[0], 0.05, 1.5)
+    assert ra.mask.sum() == 4 and np.array_equal(ra.mask, rb.mask)
+    first = rb.mask.astype(bool)
+    ra, rb = a.step(norms[1], 0.05, 1.5), b.step(norms[1], 0.05, 1.5)
+    assert ra.stats["n_trig"] == U and rb.stats["n_trig"] == U
+    assert ra.mask.sum() == 4 and rb.mask.sum() == 8
+    assert np.all(rb.mask[first] == 1)
+
+@pytest.mark.parametrize("max_o", [0, 3])
+def test_warmup_all_recover_then_normal(max_o):
+    rng = np.random.default_rng(21)
+    U, T, W = 12, 30, 5
+    rec = np.ones(U, bool)
+    rec[[2, 7]] = False
+    norms = np.exp(rng.normal(scale=0.3, size=(T, U)))
+    norms[W - 1, 4] *= 8.0                      # a trigger in the last warm-up step
+    warm = Controller(U, 5, max_o, 4, 1e-12, recoverable=rec, warmup_steps=W)
+    plain = Controller(U, 5, max_o, 4, 1e-12, recoverable=rec)
+    for t in range(1, T + 1):
+        rw, rp = warm.step(norms[t - 1], 1.3, 1.5), plain.step(norms[t - 1], 1.3, 1.5)
+        for f in ("norm", "gnmr", "dgnmr", "risk"):               # statistics untouched
+            assert np.array_equal(getattr(rw, f), getattr(rp, f))
+        if t <= W:
+            assert np.array_equal(rw.mask.astype(bool), rec)        # everyone recovers
+            assert rw.stats["n_active"] == rec.sum() and rw.stats["hit_maxo"] == 0
+        else:
+            assert rw.mask.sum() <= max_o
+    # the lock of the warm-up trigger carries over: Alg. 2's rule on A_W = B_rec
+    w2 = Controller(U, 5, max_o, 4, 1e-12, recoverable=rec, warmup_steps=W)
+    for t in range(1, W + 1):
+        r = w2.step(norms[t - 1], 1.3, 1.5)
+    assert r.lock[4] == 4 and r.risk[4] > 1.0
