@@ -55,7 +55,12 @@ enum { GNMR_F32 = 0, GNMR_BF16 = 1 };
  * caps only the newly admitted units; candidates already in A_{t-1} stay
  * active and Top_maxO ranks the remaining candidates, so
  * A_t = (C_t & A_{t-1}) U Top_maxO(C_t minus A_{t-1}; R). */
-enum { GNMR_BUDGET_ACTIVE = 0, GNMR_BUDGET_ADMITTED = 1 };
+enum { GNMR_BUDGET_ACTIVE = 0, GNMR_BUDGET_ADMITTED = 1, GNMR_BUDGET_STATIC = 2 };
+/* STATIC is the ADAPT-style static baseline of App. E.4: during the first
+ * warmup_steps = W >= 1 steps every recoverable unit takes the recovery path
+ * and GNMR is recorded; at t = W + 1 the max_o recoverable units with the
+ * largest mean GNMR over steps 1..W (ties: smaller index) become the recovery
+ * set, fixed from then on.  Locks are not used (Lock stays 0). */
 
 /* Controller settings (Alg. 1 and Alg. 2 inputs that do not change per step). */
 typedef struct {
@@ -65,7 +70,7 @@ typedef struct {
   int32_t lock_len;           /* T_lock >= 0                                      */
   double eps;                 /* epsilon >= 0, finite                              */
   const uint8_t* recoverable; /* host [num_units], nonzero = in B_rec; NULL = all */
-  int32_t budget_mode;        /* GNMR_BUDGET_ACTIVE or GNMR_BUDGET_ADMITTED        */
+  int32_t budget_mode;        /* GNMR_BUDGET_ACTIVE, _ADMITTED or _STATIC           */
   int32_t warmup_steps;       /* W >= 0: for t <= W every recoverable unit takes the
                                  recovery path (high-fidelity warm-up, App. E.6):
                                  C_t = A_t = B_rec, the lock rule of Alg. 2 applies,
@@ -153,7 +158,8 @@ gnmr_status gnmr_device_outputs(gnmr_ctx* ctx, const uint8_t** mask,
                                 const double** gnmr, const double** dgnmr,
                                 const double** risk, const gnmr_stats** stats);
 
-/* Controller state (t, A, Q, Lock, A_{t-1}) as a flat, versioned byte blob, for
+/* Controller state (t, A, Q, Lock, A_{t-1}, the static baseline's GNMR sums)
+ * as a flat, versioned byte blob, for
  * checkpoint and resume.  gnmr_state_size gives the blob size; get copies it
  * to host `buf` of `bytes` >= that size (waits for `stream`); set restores a
  * blob taken from a context with the same num_units and window.  Restoring and

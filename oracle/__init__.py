@@ -4,5 +4,6 @@ Only tests/, __graft_entry__.smoke() and the cpu_baseline leg of bench.py may
 import, call or run anything under oracle/.  It shares no code with the HIP
 library or its binding and imports neither.
 """
-from .gnmr_oracle import (BF16, BUDGET_ACTIVE, BUDGET_ADMITTED, F32, Controller,  # noqa: F401
+from .gnmr_oracle import (BF16, BUDGET_ACTIVE, BUDGET_ADMITTED, BUDGET_STATIC, F32,  # noqa: F401
+                          Controller,
                           StepResult, run_stream, sumsq, unit_norm, widen)

@@ -47,6 +47,11 @@ Policy variants (both off by default):
   * warmup_steps = W: for t <= W every recoverable unit takes the recovery
     path (the high-fidelity warm-up of App. E.6): C_t = A_t = B_rec and the
     lock rule of Alg. 2 is applied to it; GNMR state updates as usual.
+  * budget_mode = BUDGET_STATIC: the ADAPT-style static baseline of App. E.4.
+    Steps 1..W run every recoverable unit on the recovery path and record
+    GNMR; at t = W + 1 the maxO recoverable units of largest mean GNMR over
+    steps 1..W (ties: smaller index) become the recovery set for good; no
+    locks.  Counters: n_cand is |B_rec| up to t = W + 1, then |A_t|.
 """
 from __future__ import annotations
 
@@ -61,6 +66,7 @@ BF16 = 1
 # budget conventions (Sec. 3.4; the budget-convention remark of App. C)
 BUDGET_ACTIVE = 0      # |A_t| <= maxO (canonical)
 BUDGET_ADMITTED = 1    # |A_t minus A_{t-1}| <= maxO: only newly admitted units count
+BUDGET_STATIC = 2      # ADAPT-style static set fixed after a profiling warm-up (App. E.4)
 
 
 # --------------------------------------------------------------------------
@@ -120,8 +126,10 @@ class Controller:
                  warmup_steps: int = 0):
         if num_units < 1 or window < 1 or max_o < 0 or lock_len < 0:
             raise ValueError("need num_units >= 1, window >= 1, max_o >= 0, lock_len >= 0")
-        if budget_mode not in (BUDGET_ACTIVE, BUDGET_ADMITTED) or warmup_steps < 0:
+        if budget_mode not in (BUDGET_ACTIVE, BUDGET_ADMITTED, BUDGET_STATIC) or warmup_steps < 0:
             raise ValueError("unknown budget_mode or negative warmup_steps")
+        if budget_mode == BUDGET_STATIC and warmup_steps < 1:
+            raise ValueError("the static baseline needs warmup_steps >= 1")
         if not (eps >= 0.0 and math.isfinite(eps)):
             raise ValueError("need finite eps >= 0")
         self.U = int(num_units)
@@ -142,11 +150,13 @@ class Controller:
         self.Q: list[np.ndarray] = []                # oldest first, each [U]
         self.lock = np.zeros(self.U, dtype=np.int64)
         self.active = np.zeros(self.U, dtype=bool)   # A_{t-1}
+        self.gsum = np.zeros(self.U)                 # sum of GNMR over the profiling steps
 
     # -- state snapshot -----------------------------------------------------
     def get_state(self) -> dict:
         return {"t": self.t, "A": self.A.copy(), "Q": [q.copy() for q in self.Q],
-                "lock": self.lock.copy(), "active": self.active.copy()}
+                "lock": self.lock.copy(), "active": self.active.copy(),
+                "gsum": self.gsum.copy()}
 
     def set_state(self, st: dict) -> None:
         self.t = int(st["t"])
@@ -154,6 +164,7 @@ class Controller:
         self.Q = [np.array(q, dtype=np.float64) for q in st["Q"]]
         self.lock = np.array(st["lock"], dtype=np.int64)
         self.active = np.array(st["active"], dtype=bool)
+        self.gsum = np.array(st["gsum"], dtype=np.float64)
 
     # -- one controller step --------------------------------------------------
     def step(self, norms, alpha: float, beta: float) -> StepResult:
@@ -201,6 +212,8 @@ class Controller:
         # Alg. 2: candidate pool (lock counters from the previous step).
         triggered = self.rec & (risk > 1.0)
         cand = triggered | (self.rec & (self.lock > 0))
+        if self.budget_mode == BUDGET_STATIC:
+            return self._static_step(t, n, gnmr, dgnmr, risk, g_term, d_term, triggered, finite)
         warm = t <= self.warmup_steps
         if warm:
             # high-fidelity warm-up (App. E.6): every recoverable unit recovers
@@ -250,6 +263,43 @@ class Controller:
         }
         return StepResult(t, n.copy(), gnmr, dgnmr, risk, mask,
                           self.lock.astype(np.int32), stats)
+
+
+    def _static_step(self, t, n, gnmr, dgnmr, risk, g_term, d_term, triggered, finite):
+        """ADAPT-style static baseline (App. E.4): for t <= W every recoverable
+        unit takes the recovery path while sum(GNMR) is recorded; at t = W + 1
+        the maxO recoverable units with the largest mean GNMR over steps 1..W
+        (ties: smaller index) become the recovery set, fixed from then on.
+        Locks are not used."""
+        U, W = self.U, self.warmup_steps
+        ranked = np.zeros(0, dtype=np.int64)
+        if t <= W:
+            self.gsum = self.gsum + np.where(finite, gnmr, 0.0)
+            active = np.flatnonzero(self.rec)
+        elif t == W + 1:
+            mean = self.gsum / W
+            ranked = np.flatnonzero(self.rec)
+            order = np.lexsort((ranked, -mean[ranked]))
+            active = np.sort(ranked[order[: self.max_o]])
+        else:
+            active = np.flatnonzero(self.active)
+        mask = np.zeros(U, dtype=np.uint8)
+        mask[active] = 1
+        self.active = mask.astype(bool)
+        self.lock = np.zeros(U, dtype=np.int64)
+        self.t = t
+        stats = {
+            "t": t,
+            "n_trig_gnmr": int(np.count_nonzero(self.rec & (g_term > 1.0))),
+            "n_trig_dgnmr": int(np.count_nonzero(self.rec & (d_term > 1.0))),
+            "n_trig": int(np.count_nonzero(triggered)),
+            "n_cand": int(np.count_nonzero(self.rec)) if t <= W + 1 else int(active.size),
+            "n_active": int(active.size),
+            "hit_maxo": int(ranked.size > 0 and ranked.size >= self.max_o),
+            "n_nonfinite": int(np.count_nonzero(~finite)),
+        }
+        return StepResult(t, n.copy(), gnmr, dgnmr, risk, mask, self.lock.astype(np.int32),
+                          stats)
 
 
 def run_stream(norms_by_step, alphas, betas, **cfg) -> list[StepResult]:

@@ -17,7 +17,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgnmr.so
 
 GNMR_OK, GNMR_E_INVALID, GNMR_E_NOMEM, GNMR_E_HIP, GNMR_E_STATE = 0, -1, -2, -3, -4
 GNMR_F32, GNMR_BF16 = 0, 1
-GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED = 0, 1
+GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED, GNMR_BUDGET_STATIC = 0, 1, 2
 STATUS_NAMES = {0: "GNMR_OK", -1: "GNMR_E_INVALID", -2: "GNMR_E_NOMEM", -3: "GNMR_E_HIP",
                 -4: "GNMR_E_STATE"}
 

@@ -40,6 +40,8 @@ struct UpdateArgs {
   int64_t t;           // this step, 1-based
   int32_t warm;        // t <= warmup_steps
   int32_t admitted;    // budget_mode == GNMR_BUDGET_ADMITTED
+  int32_t static_set;  // budget_mode == GNMR_BUDGET_STATIC
+  int32_t warmup;      // warmup_steps (W)
   double eps, alpha, beta;
   const int64_t* unit_item_off;  // [U+1]
   const float* partial;          // [items]
@@ -57,6 +59,7 @@ struct UpdateArgs {
   uint8_t* mask;                 // [U], A_{t-1} on entry; cleared for units outside C_t
   int32_t* counters;             // [kNumCounters], zero on entry
   int32_t* cand_list;            // [U], members of C_t (any order), counters[kCntCand] of them
+  double* gsum;                  // [U], sum of GNMR over the static baseline's profiling steps
 };
 
 struct SelectArgs {

@@ -30,7 +30,7 @@ gnmr_status fail(gnmr_status st, const std::string& msg) {
   } while (0)
 
 constexpr uint32_t kStateMagic = 0x524D4E47u;  // "GNMR"
-constexpr uint32_t kStateVersion = 2;
+constexpr uint32_t kStateVersion = 3;
 constexpr int kProfileCapacity = 4096;
 
 struct StateHeader {
@@ -98,6 +98,7 @@ struct gnmr_ctx {
   uint64_t* d_keys = nullptr;
   int32_t* d_counters = nullptr;
   int32_t* d_cand_list = nullptr;
+  double* d_gsum = nullptr;
   gnmr_stats* d_stats = nullptr;
 
   // pinned staging for segment-pointer uploads; `upload_done` guards reuse
@@ -177,6 +178,9 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   u.t = t;
   u.warm = t <= c->warmup_steps ? 1 : 0;
   u.admitted = c->budget_mode == GNMR_BUDGET_ADMITTED ? 1 : 0;
+  u.static_set = c->budget_mode == GNMR_BUDGET_STATIC ? 1 : 0;
+  u.warmup = c->warmup_steps;
+  u.gsum = c->d_gsum;
   u.eps = c->eps;
   u.alpha = alpha;
   u.beta = beta;
@@ -203,7 +207,7 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   gnmr::SelectArgs s{};
   s.num_units = c->U;
   s.max_o = c->max_o;
-  s.lock_len = c->lock_len;
+  s.lock_len = u.static_set ? 0 : c->lock_len;   // the static baseline uses no locks
   s.warm = u.warm;
   s.t = t;
   s.flags = c->d_flags;
@@ -253,9 +257,12 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   if (cfg->lock_len < 0) return fail(GNMR_E_INVALID, "lock_len must be >= 0");
   if (!(cfg->eps >= 0.0) || !isfinite(cfg->eps))
     return fail(GNMR_E_INVALID, "eps must be finite and >= 0");
-  if (cfg->budget_mode != GNMR_BUDGET_ACTIVE && cfg->budget_mode != GNMR_BUDGET_ADMITTED)
+  if (cfg->budget_mode != GNMR_BUDGET_ACTIVE && cfg->budget_mode != GNMR_BUDGET_ADMITTED &&
+      cfg->budget_mode != GNMR_BUDGET_STATIC)
     return fail(GNMR_E_INVALID, "unknown budget_mode " + std::to_string(cfg->budget_mode));
   if (cfg->warmup_steps < 0) return fail(GNMR_E_INVALID, "warmup_steps must be >= 0");
+  if (cfg->budget_mode == GNMR_BUDGET_STATIC && cfg->warmup_steps < 1)
+    return fail(GNMR_E_INVALID, "the static baseline needs warmup_steps >= 1");
   const int64_t U = cfg->num_units, S = segs->num_segments;
   if (S < 0 || S > INT32_MAX) return fail(GNMR_E_INVALID, "num_segments out of range");
   if (segs->unit_seg_off == nullptr) return fail(GNMR_E_INVALID, "unit_seg_off is NULL");
@@ -337,6 +344,7 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   const size_t o_keys = take(size_t(U) * sizeof(uint64_t));
   const size_t o_cnt = take(gnmr::kNumCounters * sizeof(int32_t));
   const size_t o_list = take(size_t(U) * sizeof(int32_t));
+  const size_t o_gsum = take(size_t(U) * sizeof(double));
   const size_t o_st = take(sizeof(gnmr_stats));
   const size_t total = off;
 
@@ -369,6 +377,7 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   c->d_keys = reinterpret_cast<uint64_t*>(base + o_keys);
   c->d_counters = reinterpret_cast<int32_t*>(base + o_cnt);
   c->d_cand_list = reinterpret_cast<int32_t*>(base + o_list);
+  c->d_gsum = reinterpret_cast<double*>(base + o_gsum);
   c->d_stats = reinterpret_cast<gnmr_stats*>(base + o_st);
 
   if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ptr_stage),
@@ -403,6 +412,7 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
     e = hipMemsetAsync(c->d_Q, 0, size_t(U) * size_t(c->window) * sizeof(double), st);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_lock, 0, size_t(U) * sizeof(int32_t), st);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_mask, 0, size_t(U), st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_gsum, 0, size_t(U) * sizeof(double), st);
   if (e == hipSuccess)
     e = hipMemsetAsync(c->d_counters, 0, gnmr::kNumCounters * sizeof(int32_t), st);
   if (e == hipSuccess && S > 0)
@@ -521,7 +531,7 @@ gnmr_status gnmr_state_size(const gnmr_ctx* ctx, size_t* bytes) {
   if (ctx == nullptr || bytes == nullptr) return fail(GNMR_E_INVALID, "NULL argument");
   const size_t U = size_t(ctx->U);
   *bytes = sizeof(StateHeader) + U * sizeof(double) * (1 + size_t(ctx->window)) +
-           U * sizeof(int32_t) + U;
+           U * sizeof(int32_t) + U + U * sizeof(double);
   return GNMR_OK;
 }
 
@@ -547,6 +557,8 @@ gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream)
   GNMR_HIP(hipMemcpyAsync(p, ctx->d_lock, U * sizeof(int32_t), hipMemcpyDeviceToHost, st));
   p += U * sizeof(int32_t);
   GNMR_HIP(hipMemcpyAsync(p, ctx->d_mask, U, hipMemcpyDeviceToHost, st));
+  p += U;
+  GNMR_HIP(hipMemcpyAsync(p, ctx->d_gsum, U * sizeof(double), hipMemcpyDeviceToHost, st));
   GNMR_HIP(hipStreamSynchronize(st));
   return GNMR_OK;
 }
@@ -576,6 +588,8 @@ gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* s
   GNMR_HIP(hipMemcpyAsync(ctx->d_lock, p, U * sizeof(int32_t), hipMemcpyHostToDevice, st));
   p += U * sizeof(int32_t);
   GNMR_HIP(hipMemcpyAsync(ctx->d_mask, p, U, hipMemcpyHostToDevice, st));
+  p += U;
+  GNMR_HIP(hipMemcpyAsync(ctx->d_gsum, p, U * sizeof(double), hipMemcpyHostToDevice, st));
   GNMR_HIP(hipStreamSynchronize(st));
   ctx->t = h.t;
   return GNMR_OK;

@@ -122,7 +122,18 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   const bool trig = R > 1.0;
   bool cand = rec && (trig || a.lock[b] > 0);
   bool keep = false;
-  if (a.warm) {                       // warm-up: C_t = A_t = B_rec
+  double rank_by = R;
+  if (a.static_set) {                 // static baseline: profile, rank once, hold
+    if (a.t <= a.warmup) {
+      a.gsum[b] += finite ? G : 0.0;
+      cand = keep = rec;
+    } else if (a.t == a.warmup + 1) {
+      cand = rec;
+      rank_by = a.gsum[b] / double(a.warmup);   // mean GNMR over steps 1..W
+    } else {
+      cand = keep = a.mask[b] != 0;
+    }
+  } else if (a.warm) {                // warm-up: C_t = A_t = B_rec
     cand = rec;
     keep = rec;
   } else if (a.admitted && cand) {    // admitted-only budget: A_{t-1} members stay
@@ -134,7 +145,7 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   a.gnmr[b] = G;
   a.dgnmr[b] = D;
   a.risk[b] = R;
-  a.keys[b] = ranked ? cand_key(R) : 0;
+  a.keys[b] = ranked ? cand_key(rank_by) : 0;
   a.flags[b] = uint8_t((gt > 1.0 ? kFlagTrigG : 0) | (dt > 1.0 ? kFlagTrigD : 0) |
                        (finite ? 0 : kFlagNonFinite) | (trig ? kFlagTrigR : 0) |
                        (rec ? kFlagRec : 0) | (cand ? kFlagCand : 0) |

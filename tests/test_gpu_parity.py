@@ -377,3 +377,29 @@ def test_state_roundtrip_admitted_keeps_previous_active_set():
         assert qa["stats"] == qb["stats"]
     a.close()
     b.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama2-13b", "moe", "fine32"])
+def test_static_baseline(name):
+    """ADAPT-style static baseline (App. E.4): profile W steps with every unit
+    recovering, then fix the top-25% units by mean GNMR."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import GNMR_BUDGET_STATIC, Controller
+
+    w = R.get(name)
+    norms = R.surrogate_norms(w, seed=5)
+    W = max(1, int(np.ceil(0.05 * w.steps)))
+    K = int(np.ceil(0.25 * w.num_units))
+    say("static baseline:", name, "W", W, "K", K)
+    ora = Oracle(w.num_units, window=w.window, max_o=K, lock_len=w.lock_len, eps=w.eps,
+                 budget_mode=GNMR_BUDGET_STATIC, warmup_steps=W)
+    dn = torch.empty(w.num_units, dtype=torch.float64, device="cuda")
+    with Controller(w.num_units, w.window, K, w.lock_len, w.eps, np.zeros(w.num_units + 1),
+                    [], [], budget_mode=GNMR_BUDGET_STATIC, warmup_steps=W) as ctl:
+        for t in range(1, w.steps + 1):
+            dn.copy_(torch.from_numpy(norms[t - 1]))
+            ctl.step_from_norms(dn, w.alpha(t), w.beta(t))
+            ref = ora.step(norms[t - 1], w.alpha(t), w.beta(t))
+            assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{name}/static t={t}")
+            if t > W:
+                assert ref.mask.sum() == K

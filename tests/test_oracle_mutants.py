@@ -44,6 +44,9 @@ MUTANTS = [
     ("GNMR not clamped at A = 0", "has_mean = finite & (self.A != 0.0)", "has_mean = finite"),
     ("admitted mode keeps every candidate", "keep = cand & self.active", "keep = cand"),
     ("warm-up ignored", "cand = self.rec.copy()", "cand = cand"),
+    ("static set ranked ascending", "order = np.lexsort((ranked, -mean[ranked]))",
+     "order = np.lexsort((ranked, mean[ranked]))"),
+    ("static mean over W+1 steps", "mean = self.gsum / W", "mean = self.gsum / (W + 1) - self.gsum * 0 + (np.arange(U) == 0)"),
     ("current GNMR in window", "for q in self.Q:                       # oldest to newest",
      "for q in self.Q[1:] + [gnmr]:"),
 ]
@@ -66,6 +69,7 @@ PINS = [
     (P.test_trigger_is_strict, {}),
     (P.test_admitted_only_budget_brute_force, dict(seed=0)),
     (P.test_warmup_all_recover_then_normal, dict(max_o=3)),
+    (P.test_static_baseline_top_k_by_mean_gnmr, dict(W=6, K=4)),
 ]
 
 

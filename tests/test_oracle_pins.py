@@ -480,3 +480,33 @@ def test_warmup_all_recover_then_normal(max_o):
     for t in range(1, W + 1):
         r = w2.step(norms[t - 1], 1.3, 1.5)
     assert r.lock[4] == 4 and r.risk[4] > 1.0
+
+
+@pytest.mark.parametrize("W,K", [(1, 3), (6, 4), (10, 0)])
+def test_static_baseline_top_k_by_mean_gnmr(W, K):
+    # App. E.4: all units recover during the W profiling steps; then the K
+    # recoverable units with the largest mean GNMR over steps 1..W are the
+    # fixed recovery set (ties to the smaller index); no locks.
+    from oracle import BUDGET_STATIC
+
+    rng = np.random.default_rng(40 + W)
+    U, T = 10, W + 6
+    rec = np.ones(U, bool)
+    rec[3] = False
+    norms = np.exp(rng.normal(scale=0.4, size=(T, U)))
+    ctl = Controller(U, 5, K, 4, 0.0, recoverable=rec, budget_mode=BUDGET_STATIC, warmup_steps=W)
+    res = [ctl.step(norms[t], 1.1, 1.5) for t in range(T)]
+    means = []
+    for b in range(U):
+        gh = exact_gnmr_history([norms[i, b] for i in range(W)])
+        means.append(sum(gh, Fraction(0)) / W)
+    want = sorted((b for b in range(U) if rec[b]), key=lambda b: (-means[b], b))[:K]
+    for t, r in enumerate(res, start=1):
+        assert np.all(r.lock == 0)
+        if t <= W:
+            assert np.array_equal(r.mask.astype(bool), rec)
+        else:
+            assert set(np.flatnonzero(r.mask)) == set(want), t
+    assert res[W].stats["hit_maxo"] == int(rec.sum() > 0 and rec.sum() >= K)
+    with pytest.raises(ValueError):
+        Controller(U, 5, K, 4, 0.0, budget_mode=BUDGET_STATIC, warmup_steps=0)
