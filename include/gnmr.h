@@ -182,6 +182,57 @@ gnmr_status gnmr_profile_read(gnmr_ctx* ctx, double* ms_sumsq, double* ms_update
 gnmr_status gnmr_info(const gnmr_ctx* ctx, int64_t* num_items, int64_t* item_bytes,
                       int64_t* bytes_per_step, int32_t* launches_per_step);
 
+/* ---------------------------------------------------------------------------
+ * Recovery actuator: routes each unit's saved activations to the low-cost or
+ * the recovery path chosen by the controller (Alg. 2: "use the recovery path
+ * for b" / "use the low-cost path").  Both paths are per-token fake
+ * quantisation (App. E.2 quantisation-simulated operators; Sec. 5.1 and App.
+ * E.4: token-wise low-bit saved activations): every token (row) is scaled into
+ * the format's representable range by its largest magnitude, rounded to the
+ * nearest representable value (ties to the even significand, saturating) and
+ * rescaled, in fp32: inv = fmax / amax, s = amax / fmax, y = x * inv,
+ * out = bf16_rne(round(y) * s), signs kept; an all-zero token becomes +0.
+ * GNMR_FMT_BF16 leaves the row unchanged.
+ * ------------------------------------------------------------------------- */
+enum {
+  GNMR_FMT_BF16 = 0,  /* identity (the BF16 path)                      */
+  GNMR_FMT_E2M1 = 1,  /* 4-bit, max 6                                  */
+  GNMR_FMT_E3M2 = 2,  /* 6-bit, max 28                                 */
+  GNMR_FMT_E4M3 = 3,  /* 8-bit, max 448                                */
+  GNMR_FMT_E5M2 = 4   /* 8-bit, max 57344                              */
+};
+
+/* One unit's saved activations: a row-major bf16 [rows][cols] matrix, one
+ * row per token. */
+typedef struct {
+  const void* in;   /* device, 16-byte aligned                                  */
+  void* out;        /* device, 16-byte aligned; equal to `in` (in place) or not
+                       overlapping any segment's input                           */
+  int64_t rows;     /* tokens, >= 0                                             */
+  int32_t cols;     /* features: a multiple of 8, 8 .. 16384                     */
+  int32_t unit;     /* controller unit whose mask entry picks the format, 0 .. U-1 */
+} gnmr_act_segment;
+
+typedef struct gnmr_actuator gnmr_actuator;
+
+/* Build the row work list over the segments (host array, copied; the caller
+ * may free it).  num_units bounds the unit indices.  Allocates device memory
+ * for the tables (8 B per row, 24 B per segment). */
+gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* segs,
+                                 int64_t num_segments, int32_t num_units, void* stream);
+
+/* Apply the formats: rows of unit b use fmt_recovery when d_mask[b] != 0 (b in
+ * A_t), else fmt_low.  d_mask: device [num_units] (for example the mask from
+ * gnmr_device_outputs).  Asynchronous on `stream`.  A BF16 row in place is not
+ * touched (no memory traffic). */
+gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_low,
+                         int32_t fmt_recovery, void* stream);
+
+/* Rows in the work list and bf16 bytes of all segments' inputs. */
+gnmr_status gnmr_actuator_info(const gnmr_actuator* act, int64_t* rows, int64_t* bytes);
+
+gnmr_status gnmr_actuator_destroy(gnmr_actuator* act);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* gnmr_last_error(void);
 

@@ -21,10 +21,13 @@ GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED, GNMR_BUDGET_STATIC = 0, 1, 2
 STATUS_NAMES = {0: "GNMR_OK", -1: "GNMR_E_INVALID", -2: "GNMR_E_NOMEM", -3: "GNMR_E_HIP",
                 -4: "GNMR_E_STATE"}
 
+GNMR_FMT_BF16, GNMR_FMT_E2M1, GNMR_FMT_E3M2, GNMR_FMT_E4M3, GNMR_FMT_E5M2 = 0, 1, 2, 3, 4
+
 EXPORTED = ("gnmr_init", "gnmr_destroy", "gnmr_step", "gnmr_step_from_norms", "gnmr_sumsq",
             "gnmr_query", "gnmr_device_outputs", "gnmr_state_size", "gnmr_get_state",
             "gnmr_set_state", "gnmr_set_profiling", "gnmr_profile_read", "gnmr_info",
-            "gnmr_last_error")
+            "gnmr_last_error", "gnmr_actuator_create", "gnmr_actuate", "gnmr_actuator_info",
+            "gnmr_actuator_destroy")
 
 
 class GnmrError(RuntimeError):
@@ -44,6 +47,11 @@ class gnmr_segments(ctypes.Structure):
     _fields_ = [("num_segments", ctypes.c_int64), ("unit_seg_off", ctypes.c_void_p),
                 ("seg_numel", ctypes.c_void_p), ("seg_dtype", ctypes.c_void_p),
                 ("seg_ptr", ctypes.c_void_p)]
+
+
+class gnmr_act_segment(ctypes.Structure):
+    _fields_ = [("in_", ctypes.c_void_p), ("out", ctypes.c_void_p), ("rows", ctypes.c_int64),
+                ("cols", ctypes.c_int32), ("unit", ctypes.c_int32)]
 
 
 class gnmr_stats(ctypes.Structure):
@@ -83,6 +91,10 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "gnmr_set_profiling": [P, ctypes.c_int],
         "gnmr_profile_read": [P, P, P, P, P],
         "gnmr_info": [P, P, P, P, P],
+        "gnmr_actuator_create": [P, P, I64, I32, P],
+        "gnmr_actuate": [P, P, I32, I32, P],
+        "gnmr_actuator_info": [P, P, P],
+        "gnmr_actuator_destroy": [P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -90,7 +102,6 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         fn.restype = ctypes.c_int
     lib.gnmr_last_error.argtypes = []
     lib.gnmr_last_error.restype = ctypes.c_char_p
-    del I32, I64
     _lib = lib
     return lib
 
@@ -220,6 +231,64 @@ def gnmr_info(ctx) -> dict:
 
 def gnmr_last_error() -> str:
     return load_library().gnmr_last_error().decode()
+
+
+def gnmr_actuator_create(segments, num_units, stream=None) -> ctypes.c_void_p:
+    """segments: iterable of (in, out, rows, cols, unit); in/out are device
+    pointers (ints or tensors)."""
+    ptr = lambda p: p.data_ptr() if hasattr(p, "data_ptr") else int(p)
+    segs = [gnmr_act_segment(ptr(i), ptr(o), int(r), int(c), int(u))
+            for i, o, r, c, u in segments]
+    arr = (gnmr_act_segment * max(len(segs), 1))(*segs)
+    act = ctypes.c_void_p()
+    _check(load_library().gnmr_actuator_create(ctypes.byref(act), arr, len(segs), int(num_units),
+                                               _stream(stream)))
+    return act
+
+
+def gnmr_actuate(act, d_mask, fmt_low, fmt_recovery, stream=None) -> None:
+    p = d_mask.data_ptr() if hasattr(d_mask, "data_ptr") else int(d_mask)
+    _check(load_library().gnmr_actuate(act, p, int(fmt_low), int(fmt_recovery), _stream(stream)))
+
+
+def gnmr_actuator_info(act) -> dict:
+    r, b = ctypes.c_int64(), ctypes.c_int64()
+    _check(load_library().gnmr_actuator_info(act, ctypes.byref(r), ctypes.byref(b)))
+    return {"rows": r.value, "bytes": b.value}
+
+
+def gnmr_actuator_destroy(act) -> None:
+    _check(load_library().gnmr_actuator_destroy(act))
+
+
+class Actuator:
+    """Recovery actuator over a fixed set of saved-activation segments."""
+
+    def __init__(self, segments, num_units, stream=None):
+        self.act = gnmr_actuator_create(segments, num_units, stream)
+
+    def apply(self, d_mask, fmt_low, fmt_recovery, stream=None):
+        gnmr_actuate(self.act, d_mask, fmt_low, fmt_recovery, stream)
+
+    def info(self) -> dict:
+        return gnmr_actuator_info(self.act)
+
+    def close(self):
+        if self.act is not None:
+            gnmr_actuator_destroy(self.act)
+            self.act = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class Controller:

@@ -77,6 +77,27 @@ struct SelectArgs {
   gnmr_stats* stats;
 };
 
+// K4 (actuator): one workgroup per token row; up to kK4Vpt 16-byte vectors
+// per lane, so rows of at most kK4Block * kK4Vpt * 8 bf16 features.
+constexpr int kK4Block = 256;
+constexpr int kK4Vpt = 8;
+constexpr int kK4MaxCols = kK4Block * kK4Vpt * 8;
+
+struct ActSeg {
+  const char* in;
+  char* out;
+  int32_t cols;
+  int32_t unit;
+};
+static_assert(sizeof(ActSeg) == 24, "ActSeg layout");
+
+struct RowItem {
+  int32_t seg;
+  int32_t row;
+};
+
+hipError_t launch_actuate(const RowItem* items, int64_t num_rows, const ActSeg* segs,
+                          const uint8_t* mask, int fmt_low, int fmt_rec, hipStream_t s);
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,
                         const int32_t* seg_dtype, float* partial, hipStream_t s);
 hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,

@@ -633,4 +633,117 @@ gnmr_status gnmr_info(const gnmr_ctx* ctx, int64_t* num_items, int64_t* item_byt
   return GNMR_OK;
 }
 
+// ---------------------------------------------------------------------------
+// recovery actuator
+// ---------------------------------------------------------------------------
+
+struct gnmr_actuator {
+  int device = 0;
+  int32_t num_units = 0;
+  int64_t rows = 0;
+  int64_t bytes = 0;
+  void* arena = nullptr;
+  gnmr::RowItem* d_items = nullptr;
+  gnmr::ActSeg* d_segs = nullptr;
+};
+
+gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* segs,
+                                 int64_t num_segments, int32_t num_units, void* stream) {
+  if (out == nullptr) return fail(GNMR_E_INVALID, "out is NULL");
+  *out = nullptr;
+  if (num_segments < 0 || num_segments > INT32_MAX || (num_segments > 0 && segs == nullptr))
+    return fail(GNMR_E_INVALID, "bad segment list");
+  if (num_units < 1) return fail(GNMR_E_INVALID, "num_units must be >= 1");
+  int64_t rows = 0, bytes = 0;
+  for (int64_t k = 0; k < num_segments; ++k) {
+    const gnmr_act_segment& g = segs[k];
+    const std::string at = "activation segment " + std::to_string(k) + ": ";
+    if (g.rows < 0) return fail(GNMR_E_INVALID, at + "negative rows");
+    if (g.cols < 8 || g.cols > gnmr::kK4MaxCols || g.cols % 8 != 0)
+      return fail(GNMR_E_INVALID, at + "cols must be a multiple of 8 in [8, 16384]");
+    if (g.unit < 0 || g.unit >= num_units) return fail(GNMR_E_INVALID, at + "unit out of range");
+    if (g.rows > 0) {
+      if (g.in == nullptr || g.out == nullptr) return fail(GNMR_E_INVALID, at + "NULL pointer");
+      if (reinterpret_cast<uintptr_t>(g.in) % 16 || reinterpret_cast<uintptr_t>(g.out) % 16)
+        return fail(GNMR_E_INVALID, at + "pointers must be 16-byte aligned");
+      if (g.rows > INT32_MAX) return fail(GNMR_E_INVALID, at + "too many rows");
+    }
+    rows += g.rows;
+    bytes += g.rows * int64_t(g.cols) * 2;
+  }
+  if (rows > int64_t(UINT32_MAX)) return fail(GNMR_E_INVALID, "too many rows in total");
+  std::vector<gnmr::RowItem> items;
+  items.reserve(size_t(rows));
+  std::vector<gnmr::ActSeg> dsegs(static_cast<size_t>(num_segments));
+  for (int64_t k = 0; k < num_segments; ++k) {
+    dsegs[size_t(k)] = gnmr::ActSeg{static_cast<const char*>(segs[k].in),
+                                    static_cast<char*>(segs[k].out), segs[k].cols, segs[k].unit};
+    for (int64_t r = 0; r < segs[k].rows; ++r)
+      items.push_back(gnmr::RowItem{int32_t(k), int32_t(r)});
+  }
+  gnmr_actuator* a = new (std::nothrow) gnmr_actuator;
+  if (a == nullptr) return fail(GNMR_E_NOMEM, "host allocation failed");
+  a->num_units = num_units;
+  a->rows = rows;
+  a->bytes = bytes;
+  const size_t o_items = 0;
+  const size_t o_segs = align_up(std::max<size_t>(items.size() * sizeof(gnmr::RowItem), 1), 256);
+  const size_t total = o_segs + std::max<size_t>(dsegs.size() * sizeof(gnmr::ActSeg), 1);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipGetDevice(&a->device);
+  if (e == hipSuccess) e = hipMalloc(&a->arena, total);
+  if (e != hipSuccess) {
+    a->arena = nullptr;
+    delete a;
+    return fail(GNMR_E_NOMEM, "hipMalloc of the actuator tables failed");
+  }
+  a->d_items = reinterpret_cast<gnmr::RowItem*>(static_cast<char*>(a->arena) + o_items);
+  a->d_segs = reinterpret_cast<gnmr::ActSeg*>(static_cast<char*>(a->arena) + o_segs);
+  if (!items.empty())
+    e = hipMemcpyAsync(a->d_items, items.data(), items.size() * sizeof(gnmr::RowItem),
+                       hipMemcpyHostToDevice, st);
+  if (e == hipSuccess && !dsegs.empty())
+    e = hipMemcpyAsync(a->d_segs, dsegs.data(), dsegs.size() * sizeof(gnmr::ActSeg),
+                       hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    (void)hipFree(a->arena);
+    delete a;
+    return fail(GNMR_E_HIP, std::string("actuator upload: ") + hipGetErrorString(e));
+  }
+  *out = a;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_low,
+                         int32_t fmt_recovery, void* stream) {
+  if (act == nullptr || d_mask == nullptr) return fail(GNMR_E_INVALID, "NULL argument");
+  if (fmt_low < GNMR_FMT_BF16 || fmt_low > GNMR_FMT_E5M2 || fmt_recovery < GNMR_FMT_BF16 ||
+      fmt_recovery > GNMR_FMT_E5M2)
+    return fail(GNMR_E_INVALID, "unknown format");
+  DeviceGuard g(act->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the actuator's device");
+  GNMR_HIP(gnmr::launch_actuate(act->d_items, act->rows, act->d_segs, d_mask, fmt_low,
+                                fmt_recovery, static_cast<hipStream_t>(stream)));
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_actuator_info(const gnmr_actuator* act, int64_t* rows, int64_t* bytes) {
+  if (act == nullptr) return fail(GNMR_E_INVALID, "act is NULL");
+  if (rows) *rows = act->rows;
+  if (bytes) *bytes = act->bytes;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_actuator_destroy(gnmr_actuator* act) {
+  if (act == nullptr) return GNMR_OK;
+  DeviceGuard g(act->device);
+  if (act->arena) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(act->arena);
+  }
+  delete act;
+  return GNMR_OK;
+}
+
 }  // extern "C"

@@ -1,0 +1,148 @@
+// K4, the recovery actuator for CDNA4 (gfx950): per-token fake quantisation
+// of saved activations, the format chosen per unit by the controller's mask
+// (App. E.2 quantisation-simulated operators: each token is scaled into the
+// format's representable range, rounded to the nearest representable value
+// and rescaled; Sec. 5.1 / App. E.4: token-wise low-bit saved activations).
+//
+// One workgroup per token row (up to 16384 features, held in registers):
+// amax by a max-reduction, one fp32 division each for the scale and its
+// reciprocal, then per element y = x * inv, round to the format (ties to the
+// even significand, saturating), out = bf16_rne(q * s).  A row whose unit
+// takes the BF16 path in place is left untouched without reading it.
+#include "gnmr_internal.h"
+
+namespace gnmr {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 g_cvec;
+typedef __attribute__((address_space(1))) u32x4 g_vec;
+
+struct Format {
+  int mbits;    // significand bits
+  int emin;     // exponent of the smallest normal binade
+  float fmax;   // largest finite value
+};
+
+// E2M1, E3M2, E4M3 (OCP, 448 max), E5M2 (57344 max); no inf/NaN produced.
+__device__ __forceinline__ Format format_of(int fmt) {
+  switch (fmt) {
+    case GNMR_FMT_E2M1: return Format{1, 0, 6.0f};
+    case GNMR_FMT_E3M2: return Format{2, -2, 28.0f};
+    case GNMR_FMT_E4M3: return Format{3, -6, 448.0f};
+    default: return Format{2, -14, 57344.0f};  // GNMR_FMT_E5M2
+  }
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+__device__ __forceinline__ uint32_t to_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Nearest representable value of the format to y, ties to the even
+// significand, saturating at fmax.  All steps but rintf are exact.
+__device__ __forceinline__ float round_to_format(float y, const Format& f) {
+  const float a = fabsf(y);
+  int e = int((__float_as_uint(a) >> 23) & 0xFFu) - 127;  // binade of a (any e < emin clamps)
+  e = e < f.emin ? f.emin : e;
+  const float step = __uint_as_float(uint32_t(e - f.mbits + 127) << 23);
+  const float inv_step = __uint_as_float(uint32_t(f.mbits - e + 127) << 23);
+  float q = __fmul_rn(rintf(__fmul_rn(a, inv_step)), step);
+  q = q < f.fmax ? q : f.fmax;
+  return copysignf(q, y);
+}
+
+__device__ __forceinline__ uint32_t quant_pair(uint32_t w, float inv, float s, const Format& f) {
+  const float lo = __fmul_rn(round_to_format(__fmul_rn(bf16_lo(w), inv), f), s);
+  const float hi = __fmul_rn(round_to_format(__fmul_rn(bf16_hi(w), inv), f), s);
+  return to_bf16(lo) | (to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ float max_abs_pair(uint32_t w, float m) {
+  return fmaxf(m, fmaxf(fabsf(bf16_lo(w)), fabsf(bf16_hi(w))));
+}
+
+__global__ __launch_bounds__(kK4Block) void k4_actuate(const RowItem* __restrict__ items,
+                                                       const ActSeg* __restrict__ segs,
+                                                       const uint8_t* __restrict__ mask,
+                                                       int fmt_low, int fmt_rec) {
+  const RowItem it = items[blockIdx.x];
+  const ActSeg sg = segs[it.seg];
+  const int fmt = mask[sg.unit] ? fmt_rec : fmt_low;
+  const int64_t row_off = int64_t(it.row) * sg.cols * 2;
+  if (fmt == GNMR_FMT_BF16 && sg.in == sg.out) return;  // BF16 path in place: nothing to do
+  const g_cvec* in = (const g_cvec*)(sg.in + row_off);
+  g_vec* out = (g_vec*)(sg.out + row_off);
+  const int nvec = sg.cols >> 3;
+  const int tid = threadIdx.x;
+
+  u32x4 v[kK4Vpt];
+#pragma unroll
+  for (int k = 0; k < kK4Vpt; ++k) {
+    const int i = tid + k * kK4Block;
+    v[k] = i < nvec ? __builtin_nontemporal_load(in + i) : u32x4{0u, 0u, 0u, 0u};
+  }
+  if (fmt == GNMR_FMT_BF16) {  // BF16 path out of place: a copy
+#pragma unroll
+    for (int k = 0; k < kK4Vpt; ++k) {
+      const int i = tid + k * kK4Block;
+      if (i < nvec) out[i] = v[k];
+    }
+    return;
+  }
+
+  // amax over the row (max is exact, so the reduction order is immaterial)
+  float m = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kK4Vpt; ++k) {
+    m = max_abs_pair(v[k].x, m);
+    m = max_abs_pair(v[k].y, m);
+    m = max_abs_pair(v[k].z, m);
+    m = max_abs_pair(v[k].w, m);
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+  __shared__ float red[kK4Block / 64];
+  if ((tid & 63) == 0) red[tid >> 6] = m;
+  __syncthreads();
+  const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+
+  const Format f = format_of(fmt);
+  if (amax == 0.0f) {  // an all-zero token stays zero
+#pragma unroll
+    for (int k = 0; k < kK4Vpt; ++k) {
+      const int i = tid + k * kK4Block;
+      if (i < nvec) out[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+    return;
+  }
+  const float inv = __fdiv_rn(f.fmax, amax);  // scale into the format's range
+  const float s = __fdiv_rn(amax, f.fmax);    // and back
+#pragma unroll
+  for (int k = 0; k < kK4Vpt; ++k) {
+    const int i = tid + k * kK4Block;
+    if (i < nvec) {
+      u32x4 o;
+      o.x = quant_pair(v[k].x, inv, s, f);
+      o.y = quant_pair(v[k].y, inv, s, f);
+      o.z = quant_pair(v[k].z, inv, s, f);
+      o.w = quant_pair(v[k].w, inv, s, f);
+      out[i] = o;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_actuate(const RowItem* items, int64_t num_rows, const ActSeg* segs,
+                          const uint8_t* mask, int fmt_low, int fmt_rec, hipStream_t s) {
+  if (num_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k4_actuate, dim3(unsigned(num_rows)), dim3(kK4Block), 0, s, items, segs,
+                     mask, fmt_low, fmt_rec);
+  return hipGetLastError();
+}
+
+}  // namespace gnmr

@@ -67,3 +67,19 @@ def test_two_stage_schedule():
 
     assert [two_stage_alpha(t, 256) for t in (1, 7, 8, 256)] == [1.5, 1.5, 1.1, 1.1]
     assert two_stage_alpha(1, 16) == 1.5 and two_stage_alpha(2, 16) == 1.1
+
+
+@pytest.mark.parametrize("bad", [
+    dict(cols=12), dict(cols=0), dict(cols=16392), dict(unit=5), dict(unit=-1), dict(rows=-1),
+    dict(in_=8), dict(out=0),
+])
+def test_actuator_rejects_bad_segments(bad):
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    seg = dict(in_=4096, out=8192, rows=4, cols=64, unit=1)
+    seg.update(bad)
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_actuator_create([(seg["in_"], seg["out"], seg["rows"], seg["cols"], seg["unit"])],
+                               num_units=5)
+    assert e.value.status == B.GNMR_E_INVALID

@@ -1,0 +1,83 @@
+"""The recovery actuator (per-token fake quantisation switched by the
+controller's mask) against its oracle, bit for bit, through the C ABI."""
+import numpy as np
+import pytest
+
+from gpu_util import require_gpu
+from oracle import fakequant as FQ
+
+pytestmark = pytest.mark.gpu
+
+COLS = [8, 16, 1000, 4096, 11008, 16384, 24]
+ROWS = [3, 1, 7, 5, 2, 4, 0]
+
+
+def activations(rng):
+    out = []
+    for r, c in zip(ROWS, COLS):
+        x = rng.normal(size=(r, c)).astype(np.float32) * (10.0 ** rng.uniform(-6, 2, (r, 1)))
+        if r >= 3:
+            x[1] = 0.0                                   # an all-zero token
+            x[2, ::5] = -0.0                             # signed zeros inside a token
+            x[2, 3] = 1e4                                # an outlier
+        out.append(FQ.f32_to_bf16(x.astype(np.float32)))
+    return out
+
+
+def to_device(torch, a):
+    t = torch.from_numpy(a.view(np.int16).copy()).to("cuda")
+    assert t.data_ptr() % 16 == 0
+    return t
+
+
+@pytest.mark.parametrize("fmts", [(1, 0), (1, 3), (2, 0), (4, 2), (3, 1), (0, 0)])
+@pytest.mark.parametrize("inplace", [False, True])
+def test_actuator_matches_oracle(fmts, inplace):
+    torch = require_gpu()
+    from paper_2606_00539_amd import Actuator
+
+    rng = np.random.default_rng(sum(fmts) * 7 + inplace)
+    acts = activations(rng)
+    U = len(acts)
+    mask = (rng.random(U) < 0.5).astype(np.uint8)
+    d_in = [to_device(torch, a) for a in acts]
+    d_out = d_in if inplace else [torch.full_like(t, 0x5555) for t in d_in]
+    d_mask = torch.from_numpy(mask).to("cuda")
+    segs = [(i, o, a.shape[0], a.shape[1], b) for b, (i, o, a) in enumerate(zip(d_in, d_out, acts))]
+    with Actuator(segs, U) as act:
+        info = act.info()
+        assert info["rows"] == sum(ROWS)
+        act.apply(d_mask, *fmts)
+        torch.cuda.synchronize()
+    want = FQ.actuate(acts, mask, *fmts)
+    for b, (o, w) in enumerate(zip(d_out, want)):
+        got = o.cpu().numpy().view(np.uint16).reshape(w.shape)
+        bad = np.argwhere(got != w)
+        assert bad.size == 0, f"unit {b} fmt {fmts}: {len(bad)} differ, first {bad[:3].tolist()}"
+
+
+def test_actuator_follows_the_controller_mask():
+    """Zero-copy: the controller's device mask drives the actuator directly."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import GNMR_FMT_BF16, GNMR_FMT_E2M1, Actuator, Controller
+
+    U = 6
+    rng = np.random.default_rng(5)
+    acts = [FQ.f32_to_bf16(rng.normal(size=(16, 4096)).astype(np.float32)) for _ in range(U)]
+    d_in = [to_device(torch, a) for a in acts]
+    norms = torch.ones(U, dtype=torch.float64, device="cuda")
+    with Controller(U, 5, 2, 1, 0.0, np.zeros(U + 1), [], []) as ctl, \
+            Actuator([(t, t, 16, 4096, b) for b, t in enumerate(d_in)], U) as act:
+        for _ in range(6):
+            ctl.step_from_norms(norms, 1.1, 1.5)
+        norms[[1, 4]] = 9.0                        # two units spike -> recovery path
+        ctl.step_from_norms(norms, 1.1, 1.5)
+        dmask = ctl.device_outputs()["mask"]
+        act.apply(dmask, GNMR_FMT_E2M1, GNMR_FMT_BF16)
+        torch.cuda.synchronize()
+        mask = ctl.query()["mask"]
+    assert mask.tolist() == [0, 1, 0, 0, 1, 0]
+    for b in range(U):
+        got = d_in[b].cpu().numpy().view(np.uint16).reshape(16, 4096)
+        want = acts[b] if mask[b] else FQ.fakequant_rows(acts[b], GNMR_FMT_E2M1)
+        assert np.array_equal(got, want)

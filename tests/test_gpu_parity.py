@@ -14,6 +14,7 @@ import streams as S
 from gpu_util import assert_step_matches, controller_for, device_buffer, require_gpu
 from oracle import Controller as Oracle
 from oracle import sumsq as oracle_sumsq
+from oracle import unit_norm as oracle_norm
 from synth import layout as L
 from synth import recipe as R
 from synth import values as V
@@ -403,3 +404,47 @@ def test_static_baseline(name):
             assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{name}/static t={t}")
             if t > W:
                 assert ref.mask.sum() == K
+
+
+def test_torch_units_on_a_model():
+    """Gradients of a small LLaMA-style block stack registered by name; one
+    unit per projection weight and one block-as-unit variant."""
+    torch = require_gpu()
+    from paper_2606_00539_amd.torch_units import TorchUnits, llama_linear_units
+
+    torch.manual_seed(0)
+    d, f = 96, 160
+
+    def block():
+        return torch.nn.ModuleDict({n: torch.nn.Linear(*s, bias=False) for n, s in (
+            ("q_proj", (d, d)), ("k_proj", (d, d)), ("v_proj", (d, d)), ("o_proj", (d, d)),
+            ("gate_proj", (d, f)), ("up_proj", (d, f)), ("down_proj", (f, d)))})
+
+    model = torch.nn.ModuleDict({"layers": torch.nn.ModuleList([block(), block()])})
+    model = model.to("cuda", torch.bfloat16)
+    params = list(model.named_parameters())
+    per_op = TorchUnits(params, max_o=2, lock_len=2, unit_of=llama_linear_units)
+    per_block = TorchUnits(params, max_o=1, lock_len=2,
+                           unit_of=lambda n: ".".join(n.split(".")[:2]))
+    assert len(per_op.unit_names) == 14 and per_block.unit_names == ["layers.0", "layers.1"]
+    ora_op = Oracle(14, window=5, max_o=2, lock_len=2, eps=1e-12)
+    ora_blk = Oracle(2, window=5, max_o=1, lock_len=2, eps=1e-12)
+    gen = torch.Generator(device="cuda").manual_seed(1)
+    for t in range(1, 13):
+        for i, (name, p) in enumerate(params):
+            scale = 1e-3 * (20.0 if (t == 9 and i == 4) else 1.0)
+            p.grad = (torch.randn(p.shape, device="cuda", generator=gen) * scale).to(p.dtype)
+        per_op.step(1.1, 1.5)
+        per_block.step(1.1, 1.5)
+        host = {n: p.grad.view(torch.int16).cpu().numpy().view(np.uint16) for n, p in params}
+        n_op = [oracle_norm([(host[n], 1)]) for n in per_op.param_names]
+        n_blk = [oracle_norm([(host[n], 1) for n in per_block.param_names if n.startswith(u + ".")])
+                 for u in per_block.unit_names]
+        for ctl, ora, norms in ((per_op, ora_op, n_op), (per_block, ora_blk, n_blk)):
+            ref = ora.step(norms, 1.1, 1.5)
+            assert_step_matches(ctl.query(), ref, rtol=1e-5, what=f"torch units t={t}")
+        if t == 9:   # the spiked projection and its block go to the recovery path
+            assert "layers.0.gate_proj" in per_op.recovery_set()
+            assert per_block.recovery_set() == ["layers.0"]
+    per_op.close()
+    per_block.close()
