@@ -115,6 +115,60 @@ def copy_probe(torch, nbytes: int, steps: int, warmup: int) -> None:
                       "read_plus_write_GBs": round(2 * nbytes / dt / 1e9, 1)}), flush=True)
 
 
+def actuator_bench(torch, tokens: int, steps: int, warmup: int) -> None:
+    """Saved activations of the 7 projections of each of 32 LLaMA-2-7B layers
+    for `tokens` tokens (q, k, v, o, gate, up inputs: 4096 features; down:
+    11008), all on the low-cost path (E2M1, in place): every byte is read and
+    written once.  Also times the mixed case of 8 units on the BF16 path."""
+    import numpy as np
+
+    from paper_2606_00539_amd import GNMR_FMT_BF16, GNMR_FMT_E2M1, Actuator
+
+    cols = [4096] * 6 + [11008]
+    U = 32 * 7
+    shapes = [(tokens, cols[b % 7]) for b in range(U)]
+    total = sum(r * c for r, c in shapes)
+    buf = torch.randn(total, dtype=torch.bfloat16, device="cuda")
+    segs, off = [], 0
+    for b, (r, c) in enumerate(shapes):
+        p = buf.data_ptr() + 2 * off
+        segs.append((p, p, r, c, b))
+        off += r * c
+    act = Actuator(segs, U)
+    nbytes = act.info()["bytes"]
+    results = {}
+    for label, nrec in (("all_low_cost", 0), ("maxO8_bf16_in_place", 8)):
+        mask = np.zeros(U, np.uint8)
+        mask[np.random.default_rng(0).choice(U, nrec, replace=False)] = 1
+        d_mask = torch.from_numpy(mask).to("cuda")
+        for _ in range(warmup):
+            act.apply(d_mask, GNMR_FMT_E2M1, GNMR_FMT_BF16)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            act.apply(d_mask, GNMR_FMT_E2M1, GNMR_FMT_BF16)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        moved = 2 * sum(r * c * 2 for (r, c), m in zip(shapes, mask) if not m)
+        results[label] = {"ms": round(ms, 4), "bytes_moved": moved,
+                          "GBs": round(moved / (ms * 1e-3) / 1e9, 1)}
+    a = results["all_low_cost"]
+    print(json.dumps({
+        "metric": "recovery actuator GB/s (bf16 read + write, per-token E2M1 fake quantisation)",
+        "value": a["GBs"], "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": a["ms"], "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"LLaMA-2-7B-shaped saved activations, 224 units, {tokens} "
+                               f"tokens, {nbytes / 1e9:.2f} GB bf16", "units": U,
+                   "tokens": tokens, "activation_bytes": nbytes},
+        "roofline": {"bound": "hbm", "achieved": a["GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(a["GBs"] / HBM_PEAK_GBS, 4), "kernel": "k4_actuate",
+                     "algorithmic_bytes": a["bytes_moved"]},
+        "cases": results}), flush=True)
+    act.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,6 +176,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama2-13b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--actuator", action="store_true",
+                    help="measure the recovery actuator (per-token fake quantisation of "
+                         "LLaMA-2-7B-shaped saved activations) instead of the controller")
+    ap.add_argument("--tokens", type=int, default=4096)
     ap.add_argument("--probe-copy-bytes", type=float, default=0,
                     help="instead of the controller, time device-to-device copies of this "
                          "many bytes (the known-size reference for HBM byte counters)")
@@ -143,6 +201,9 @@ def main():
     torch.cuda.set_device(0)
     if args.probe_copy_bytes:
         copy_probe(torch, int(args.probe_copy_bytes), args.steps, args.warmup)
+        return
+    if args.actuator:
+        actuator_bench(torch, args.tokens, args.steps, args.warmup)
         return
     w = R.get(args.workload)
     lay = L.for_workload(w)
