@@ -127,13 +127,18 @@ gnmr_status gnmr_destroy(gnmr_ctx* ctx);
  * alpha_t, beta_t > 0 and finite (values below 1 are legal).  seg_ptr: host
  * [S] of device pointers for this step, or NULL to reuse the last bound ones.
  * Asynchronous: only enqueues work on `stream`.  The gradient buffers must
- * stay valid and unmodified until that work is done. */
+ * stay valid and unmodified until that work is done.
+ * HIP graphs: with seg_ptr == NULL (pointers bound before) and profiling off,
+ * a step enqueues kernels only (no allocation, copy or memset) and can be
+ * captured; the step counter lives on the device, so every replay performs
+ * the next step.  alpha_t and beta_t are fixed at capture time. */
 gnmr_status gnmr_step(gnmr_ctx* ctx, double alpha_t, double beta_t,
                       const void* const* seg_ptr, void* stream);
 
 /* The same step with the norms given: d_norm is device [num_units] float64
  * n_{b,t}; the gradient pass is skipped.  For callers that already hold the
- * norms (and for testing the state update and selection alone). */
+ * norms (and for testing the state update and selection alone).  Capturable
+ * in a HIP graph like gnmr_step. */
 gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm,
                                  double alpha_t, double beta_t, void* stream);
 

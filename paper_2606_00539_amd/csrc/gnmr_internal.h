@@ -35,13 +35,10 @@ enum : uint8_t {
 struct UpdateArgs {
   int32_t num_units;
   int32_t window;      // delta
-  int32_t qlen;        // values in Q before this step (min(t-1, delta))
-  int32_t slot;        // ring slot of the oldest value == slot of the new value
-  int64_t t;           // this step, 1-based
-  int32_t warm;        // t <= warmup_steps
   int32_t admitted;    // budget_mode == GNMR_BUDGET_ADMITTED
   int32_t static_set;  // budget_mode == GNMR_BUDGET_STATIC
   int32_t warmup;      // warmup_steps (W)
+  const int64_t* step; // steps completed so far (device); this step is *step + 1
   double eps, alpha, beta;
   const int64_t* unit_item_off;  // [U+1]
   const float* partial;          // [items]
@@ -66,8 +63,8 @@ struct SelectArgs {
   int32_t num_units;
   int32_t max_o;
   int32_t lock_len;
-  int32_t warm;
-  int64_t t;
+  int32_t warmup;      // warmup_steps (W)
+  int64_t* step;       // steps completed (device); advanced by one at the end of K3
   const uint8_t* flags;
   const uint64_t* keys;
   int32_t* counters;         // from K2; reset to zero for the next step

@@ -76,7 +76,6 @@ struct gnmr_ctx {
   std::vector<int32_t> seg_dtype;
   int64_t num_items = 0;
   int64_t bytes_per_step = 0;
-  int64_t t = 0;               // steps completed
   bool ptrs_bound = false;
 
   void* arena = nullptr;
@@ -100,6 +99,7 @@ struct gnmr_ctx {
   int32_t* d_cand_list = nullptr;
   double* d_gsum = nullptr;
   gnmr_stats* d_stats = nullptr;
+  int64_t* d_step = nullptr;   // steps completed (advanced by K3)
 
   // pinned staging for segment-pointer uploads; `upload_done` guards reuse
   const void** h_ptr_stage = nullptr;
@@ -169,17 +169,13 @@ gnmr_status record(gnmr_ctx* c, int which, hipStream_t st) {
 // K2 + K3 for step t+1 (K1 already enqueued when ext_norm is null).
 gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha, double beta,
                               hipStream_t st) {
-  const int64_t t = c->t + 1;
   gnmr::UpdateArgs u{};
   u.num_units = c->U;
   u.window = c->window;
-  u.qlen = int32_t(std::min<int64_t>(t - 1, c->window));
-  u.slot = int32_t((t - 1) % c->window);
-  u.t = t;
-  u.warm = t <= c->warmup_steps ? 1 : 0;
   u.admitted = c->budget_mode == GNMR_BUDGET_ADMITTED ? 1 : 0;
   u.static_set = c->budget_mode == GNMR_BUDGET_STATIC ? 1 : 0;
   u.warmup = c->warmup_steps;
+  u.step = c->d_step;
   u.gsum = c->d_gsum;
   u.eps = c->eps;
   u.alpha = alpha;
@@ -208,8 +204,8 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   s.num_units = c->U;
   s.max_o = c->max_o;
   s.lock_len = u.static_set ? 0 : c->lock_len;   // the static baseline uses no locks
-  s.warm = u.warm;
-  s.t = t;
+  s.warmup = c->warmup_steps;
+  s.step = c->d_step;
   s.flags = c->d_flags;
   s.keys = c->d_keys;
   s.counters = c->d_counters;
@@ -220,7 +216,6 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   GNMR_HIP(gnmr::launch_select(s, st));
   r = record(c, 3, st);
   if (r != GNMR_OK) return r;
-  c->t = t;
   if (c->prof && c->prof_steps < kProfileCapacity) ++c->prof_steps;
   return GNMR_OK;
 }
@@ -346,6 +341,7 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   const size_t o_list = take(size_t(U) * sizeof(int32_t));
   const size_t o_gsum = take(size_t(U) * sizeof(double));
   const size_t o_st = take(sizeof(gnmr_stats));
+  const size_t o_step = take(sizeof(int64_t));
   const size_t total = off;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -379,6 +375,7 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   c->d_cand_list = reinterpret_cast<int32_t*>(base + o_list);
   c->d_gsum = reinterpret_cast<double*>(base + o_gsum);
   c->d_stats = reinterpret_cast<gnmr_stats*>(base + o_st);
+  c->d_step = reinterpret_cast<int64_t*>(base + o_step);
 
   if (hipHostMalloc(reinterpret_cast<void**>(&c->h_ptr_stage),
                     std::max<size_t>(size_t(S), 1) * sizeof(void*), hipHostMallocDefault) !=
@@ -413,6 +410,8 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   if (e == hipSuccess) e = hipMemsetAsync(c->d_lock, 0, size_t(U) * sizeof(int32_t), st);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_mask, 0, size_t(U), st);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_gsum, 0, size_t(U) * sizeof(double), st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_stats, 0, sizeof(gnmr_stats), st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->d_step, 0, sizeof(int64_t), st);
   if (e == hipSuccess)
     e = hipMemsetAsync(c->d_counters, 0, gnmr::kNumCounters * sizeof(int32_t), st);
   if (e == hipSuccess && S > 0)
@@ -493,7 +492,6 @@ gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr, double* d_sums
 gnmr_status gnmr_query(gnmr_ctx* ctx, uint8_t* mask, int32_t* lock, double* norm, double* gnmr,
                        double* dgnmr, double* risk, gnmr_stats* stats, void* stream) {
   if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
-  if (ctx->t == 0) return fail(GNMR_E_STATE, "no step has been taken yet");
   DeviceGuard g(ctx->device);
   if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -508,8 +506,11 @@ gnmr_status gnmr_query(gnmr_ctx* ctx, uint8_t* mask, int32_t* lock, double* norm
   GNMR_HIP(d2h(gnmr, ctx->d_gnmr, U * sizeof(double)));
   GNMR_HIP(d2h(dgnmr, ctx->d_dgnmr, U * sizeof(double)));
   GNMR_HIP(d2h(risk, ctx->d_risk, U * sizeof(double)));
-  GNMR_HIP(d2h(stats, ctx->d_stats, sizeof(gnmr_stats)));
+  gnmr_stats local;
+  GNMR_HIP(d2h(&local, ctx->d_stats, sizeof(gnmr_stats)));
   GNMR_HIP(hipStreamSynchronize(st));
+  if (local.t == 0) return fail(GNMR_E_STATE, "no step has been taken yet");
+  if (stats) *stats = local;
   return GNMR_OK;
 }
 
@@ -543,7 +544,10 @@ gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream)
   DeviceGuard g(ctx->device);
   if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  StateHeader h{kStateMagic, kStateVersion, ctx->U, ctx->window, ctx->t,
+  int64_t t = 0;
+  GNMR_HIP(hipMemcpyAsync(&t, ctx->d_step, sizeof(int64_t), hipMemcpyDeviceToHost, st));
+  GNMR_HIP(hipStreamSynchronize(st));
+  StateHeader h{kStateMagic, kStateVersion, ctx->U, ctx->window, t,
                 ctx->max_o, ctx->lock_len, ctx->eps};
   char* p = static_cast<char*>(buf);
   memcpy(p, &h, sizeof h);
@@ -590,8 +594,8 @@ gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* s
   GNMR_HIP(hipMemcpyAsync(ctx->d_mask, p, U, hipMemcpyHostToDevice, st));
   p += U;
   GNMR_HIP(hipMemcpyAsync(ctx->d_gsum, p, U * sizeof(double), hipMemcpyHostToDevice, st));
+  GNMR_HIP(hipMemcpyAsync(ctx->d_step, &h.t, sizeof(int64_t), hipMemcpyHostToDevice, st));
   GNMR_HIP(hipStreamSynchronize(st));
-  ctx->t = h.t;
   return GNMR_OK;
 }
 

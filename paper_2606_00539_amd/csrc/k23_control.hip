@@ -91,16 +91,23 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   if (lane != 0) return;
 
   const int U = a.num_units;
+  // The step counter lives on the device, so that a captured step replays
+  // correctly: t = 1 + steps completed, the queue holds min(t - 1, delta)
+  // values, and the oldest value sits in the slot the new one replaces.
+  const int64_t t = *a.step + 1;
+  const int qlen = t - 1 < a.window ? int(t - 1) : a.window;
+  const int slot0 = int((t - 1) % a.window);
+  const bool warm = t <= a.warmup;
   const bool finite = isfinite(n);
   const double A_prev = a.A[b];
   // Alg. 1: GNMR = 1 at t = 1 or while the historical mean is 0.
   double G = 1.0;
-  if (finite && a.t > 1 && A_prev != 0.0) G = n / (A_prev + a.eps);
+  if (finite && t > 1 && A_prev != 0.0) G = n / (A_prev + a.eps);
   // Alg. 1: Delta-GNMR once the queue holds delta values, oldest first.
   double D = 1.0;
-  if (a.qlen == a.window) {
+  if (qlen == a.window) {
     double total = 0.0;
-    int slot = a.slot;
+    int slot = slot0;
     for (int j = 0; j < a.window; ++j) {
       total += a.Q[int64_t(slot) * U + b];
       slot = slot + 1 == a.window ? 0 : slot + 1;
@@ -109,8 +116,8 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
     if (finite && den != 0.0) D = G / den;
   }
   // Alg. 1: running mean and queue push (the new value replaces the oldest).
-  if (finite) a.A[b] = A_prev + (n - A_prev) / double(a.t);
-  a.Q[int64_t(a.slot) * U + b] = finite ? G : 1.0;
+  if (finite) a.A[b] = A_prev + (n - A_prev) / double(t);
+  a.Q[int64_t(slot0) * U + b] = finite ? G : 1.0;
   if (!finite) G = D = INFINITY;
 
   // Alg. 2: R = max(GNMR / alpha, Delta-GNMR / beta); the pool C_t holds the
@@ -124,16 +131,16 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   bool keep = false;
   double rank_by = R;
   if (a.static_set) {                 // static baseline: profile, rank once, hold
-    if (a.t <= a.warmup) {
+    if (t <= a.warmup) {
       a.gsum[b] += finite ? G : 0.0;
       cand = keep = rec;
-    } else if (a.t == a.warmup + 1) {
+    } else if (t == a.warmup + 1) {
       cand = rec;
       rank_by = a.gsum[b] / double(a.warmup);   // mean GNMR over steps 1..W
     } else {
       cand = keep = a.mask[b] != 0;
     }
-  } else if (a.warm) {                // warm-up: C_t = A_t = B_rec
+  } else if (warm) {                  // warm-up: C_t = A_t = B_rec
     cand = rec;
     keep = rec;
   } else if (a.admitted && cand) {    // admitted-only budget: A_{t-1} members stay
@@ -375,18 +382,21 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
   if (c_act) atomicAdd(&cnt[0], c_act);
   __syncthreads();
   if (tid == 0) {
+    const int64_t t = *a.step + 1;
+    const bool warm = t <= a.warmup;
     gnmr_stats st;
-    st.t = a.t;
+    st.t = t;
     st.n_trig_gnmr = a.counters[kCntTrigG];
     st.n_trig_dgnmr = a.counters[kCntTrigD];
     st.n_trig = a.counters[kCntTrigR];
     st.n_cand = n_cand;
     st.n_active = cnt[0];
-    st.hit_maxo = (!a.warm && n_rank > 0 && n_rank >= a.max_o) ? 1 : 0;
+    st.hit_maxo = (!warm && n_rank > 0 && n_rank >= a.max_o) ? 1 : 0;
     st.n_nonfinite = a.counters[kCntNonFinite];
     st.reserved = 0;
     *a.stats = st;
     for (int k = 0; k < kNumCounters; ++k) a.counters[k] = 0;  // ready for the next step
+    *a.step = t;
   }
 }
 

@@ -72,4 +72,7 @@ def build(unit_numel, unit_dtype, pieces=None, align: int = 256, shift=None) -> 
 
 
 def for_workload(w, align: int = 256) -> Layout:
-    return build(w.numel, w.dtypes, align=align)
+    pieces = None
+    if any(u.pieces for u in w.units):
+        pieces = [list(u.pieces) if u.pieces else [u.numel] for u in w.units]
+    return build(w.numel, w.dtypes, pieces=pieces, align=align)

@@ -31,6 +31,7 @@ class Unit:
     name: str
     numel: int
     dtype: int
+    pieces: tuple = ()      # segment lengths when the unit owns several tensors
 
 
 @dataclass
@@ -108,6 +109,13 @@ def dense_units(layers: int, d: int, ffn: int, dtype: int, row_block: int = 0) -
     return units
 
 
+def layer_units(layers: int, d: int, ffn: int, dtype: int) -> list:
+    """Block-as-unit (Sec. 3.4): each decoder layer is one unit owning its
+    seven projection weights as seven segments (q, k, v, o, gate, up, down)."""
+    pieces = (d * d,) * 4 + (ffn * d,) * 2 + (d * ffn,)
+    return [Unit(f"L{layer}", sum(pieces), dtype, pieces) for layer in range(layers)]
+
+
 def moe_units(layers: int = 27, hidden: int = 2048, expert_ffn: int = 1408,
               routed: int = 64, shared: int = 2, dtype: int = DTYPE_F32) -> list:
     units = []
@@ -164,6 +172,18 @@ def llama13b(seed: int = 0) -> Workload:
                                 f"in {per_step} units every step")
 
 
+def llama13b_layers(seed: int = 0) -> Workload:
+    """The paper's 13B controller setting: maxO = 10 over 40 decoder layers,
+    T_lock = 1, two-stage alpha 1.5 -> 1.1, beta = 1.5, window 5 (App. E.3),
+    on the LLaMA-2-13B-shaped bf16 gradient set with each layer one unit."""
+    units = layer_units(40, 5120, 13824, DTYPE_BF16)
+    scale, _ = _spiky_stream(units, 16, seed, 0, 1, [10.0, 50.0], every_step=True)
+    return Workload("llama2-13b-layers", units, 16, max_o=10, lock_len=1, seed=seed,
+                    scale64=scale,
+                    description="LLaMA-2-13B-shaped, 40 block units of 7 bf16 segments, "
+                                "x10/x50 spike in one layer every step")
+
+
 def moe(seed: int = 0) -> Workload:
     units = moe_units()
     steps = 32
@@ -211,6 +231,7 @@ WORKLOADS = {
     "tiny": tiny,
     "llama2-7b": llama7b,
     "llama2-13b": llama13b,
+    "llama2-13b-layers": llama13b_layers,
     "moe": moe,
     "fine128": lambda seed=0: fine(seed, 128),
     "fine32": lambda seed=0: fine(seed, 32),

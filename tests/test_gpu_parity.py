@@ -448,3 +448,37 @@ def test_torch_units_on_a_model():
             assert per_block.recovery_set() == ["layers.0"]
     per_op.close()
     per_block.close()
+
+
+def test_graph_captured_step_replays_match_oracle(gen):
+    """gnmr_step captured once in a HIP graph and replayed for the rest of
+    the tiny stream; fresh gradients and synchronisations between replays;
+    every replay checked against the oracle."""
+    torch = require_gpu()
+    w = R.get("tiny")
+    nudge, _, ref, alphas, betas = S.guarded_stream(
+        w, lambda t, s32, units: S.host_norms(w, t, s32, units))
+    lay = L.for_workload(w)
+    buf, base, ptrs = device_buffer(torch, lay)
+    capture_at = 5
+    assert len(set(alphas[capture_at - 1:])) == 1 and len(set(betas)) == 1
+    with controller_for(lay, w, ptrs) as ctl:
+        for t in range(1, capture_at):
+            gen.fill(lay, base, w.seed, t, w.scale32(t, nudge[t - 1]))
+            ctl.step(alphas[t - 1], betas[t - 1])
+            assert_step_matches(ctl.query(), ref[t - 1], what=f"eager t={t}")
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        gen.fill(lay, base, w.seed, capture_at, w.scale32(capture_at, nudge[capture_at - 1]))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(graph, stream=side):
+                ctl.step(alphas[capture_at - 1], betas[capture_at - 1], stream=side)
+        torch.cuda.synchronize()
+        assert ctl.query()["stats"]["t"] == capture_at - 1   # capture ran nothing
+        for t in range(capture_at, w.steps + 1):
+            if t > capture_at:
+                gen.fill(lay, base, w.seed, t, w.scale32(t, nudge[t - 1]))
+            graph.replay()
+            torch.cuda.synchronize()
+            assert_step_matches(ctl.query(), ref[t - 1], what=f"replay t={t}")

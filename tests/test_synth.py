@@ -55,6 +55,7 @@ def test_table_and_moments():
     ("tiny", 28, 3_162_112, 12_648_448),
     ("llama2-7b", 224, 6_476_005_376, 12_952_010_752),
     ("llama2-13b", 280, 12_687_769_600, 25_375_539_200),
+    ("llama2-13b-layers", 40, 12_687_769_600, 25_375_539_200),
     ("moe", 5454, 15_868_624_896, 63_474_499_584),
     ("fine128", 10624, 6_476_005_376, 12_952_010_752),
     ("fine32", 42496, 6_476_005_376, 12_952_010_752),
