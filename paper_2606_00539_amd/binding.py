@@ -71,7 +71,7 @@ _lib = None
 def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
     """Load libgnmr.so (once).  Raises if it is not built."""
     global _lib
-    if _lib is not None:
+    if _lib is not None and path == _LIB_PATH:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
@@ -102,7 +102,8 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         fn.restype = ctypes.c_int
     lib.gnmr_last_error.argtypes = []
     lib.gnmr_last_error.restype = ctypes.c_char_p
-    _lib = lib
+    if path == _LIB_PATH:
+        _lib = lib
     return lib
 
 

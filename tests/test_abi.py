@@ -83,3 +83,19 @@ def test_actuator_rejects_bad_segments(bad):
         B.gnmr_actuator_create([(seg["in_"], seg["out"], seg["rows"], seg["cols"], seg["unit"])],
                                num_units=5)
     assert e.value.status == B.GNMR_E_INVALID
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    from paper_2606_00539_amd import binding as B
+
+    with pytest.raises(RuntimeError, match="not built"):
+        B.load_library(str(tmp_path / "libgnmr.so"))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    import subprocess
+    import sys
+
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "8"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr

@@ -22,7 +22,7 @@ from synth import recipe as R
 
 pytestmark = pytest.mark.gpu
 
-E2E = ["tiny", "llama2-7b", "llama2-13b", "moe", "fine128", "fine32"]
+E2E = ["tiny", "llama2-7b", "llama2-13b", "llama2-13b-layers", "moe", "fine128", "fine32"]
 STAT_KEYS = ("t", "n_trig_gnmr", "n_trig_dgnmr", "n_trig", "n_cand", "n_active", "hit_maxo",
              "n_nonfinite")
 

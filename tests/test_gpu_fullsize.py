@@ -22,7 +22,8 @@ from synth import recipe as R
 
 pytestmark = pytest.mark.gpu
 
-FULL = [("llama2-7b", 3), ("llama2-13b", 3), ("moe", 4), ("fine128", 4), ("fine32", 4)]
+FULL = [("llama2-7b", 3), ("llama2-13b", 3), ("llama2-13b-layers", 3), ("moe", 4), ("fine128", 4),
+        ("fine32", 4)]
 
 
 def say(*a):
