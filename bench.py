@@ -176,6 +176,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama2-13b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one captured step (HIP graph) instead of eager steps; "
+                         "kernel times still come from an eager profiled pass")
     ap.add_argument("--actuator", action="store_true",
                     help="measure the recovery actuator (per-token fake quantisation of "
                          "LLaMA-2-7B-shaped saved activations) instead of the controller")
@@ -233,6 +236,21 @@ def main():
     elapsed = time.perf_counter() - t0
     prof = ctl.profile_read()
     ctl.set_profiling(False)
+    if args.graph:
+        # one step captured with the thresholds now in force, replayed K times
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(graph, stream=side):
+                ctl.step(w.alpha(t + 1), w.beta(t + 1), stream=side)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        log(f"[bench] {args.steps} graph replays in {elapsed:.6f} s")
     out = ctl.query(stream=stream)
     log(f"[bench] timed {args.steps} steps in {elapsed:.4f} s; stats {out['stats']}")
 
@@ -259,7 +277,8 @@ def main():
                    "bytes_per_step": w.bytes_per_step, "max_o": w.max_o,
                    "lock_len": w.lock_len, "window": w.window,
                    "work_items": info["num_items"], "item_bytes": info["item_bytes"],
-                   "launches_per_step": info["launches_per_step"]},
+                   "launches_per_step": info["launches_per_step"],
+                   "timing": "graph replays" if args.graph else "eager steps"},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
