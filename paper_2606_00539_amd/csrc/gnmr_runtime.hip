@@ -196,10 +196,6 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   u.mask = c->d_mask;
   u.counters = c->d_counters;
   u.cand_list = c->d_cand_list;
-  GNMR_HIP(gnmr::launch_update(u, c->num_items, st));
-  gnmr_status r = record(c, 2, st);
-  if (r != GNMR_OK) return r;
-
   gnmr::SelectArgs s{};
   s.num_units = c->U;
   s.max_o = c->max_o;
@@ -213,6 +209,9 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   s.lock = c->d_lock;
   s.mask = c->d_mask;
   s.stats = c->d_stats;
+  GNMR_HIP(gnmr::launch_update(u, c->num_items, st));
+  gnmr_status r = record(c, 2, st);
+  if (r != GNMR_OK) return r;
   GNMR_HIP(gnmr::launch_select(s, st));
   r = record(c, 3, st);
   if (r != GNMR_OK) return r;

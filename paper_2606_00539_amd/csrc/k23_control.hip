@@ -74,22 +74,12 @@ __device__ __forceinline__ uint64_t cand_key(double R) {
   return uint64_t(__double_as_longlong(R)) + 1;
 }
 
-// K2: L lanes per unit sum its partials; lane 0 then runs Alg. 1, the risk of
-// Alg. 2, and marks the unit's membership of the candidate pool C_t.
-template <int L>
-__global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
-  __shared__ double red[4];
-  const int lane = L == 1 ? 0 : int(threadIdx.x % L);
-  const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
-  if (b >= a.num_units) return;  // uniform per workgroup when L = 256
-  double n;
-  if (a.ext_norm != nullptr) {
-    n = a.ext_norm[b];
-  } else {
-    n = sqrt(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
-  }
-  if (lane != 0) return;
-
+// Alg. 1 and the risk of Alg. 2 for unit b given its norm n, and the unit's
+// membership of the candidate pool C_t.  kWaveAgg: every lane of the
+// wavefront handles its own unit and the counters are aggregated by ballot;
+// otherwise one lane calls this for its unit alone.
+template <bool kWaveAgg>
+__device__ __forceinline__ void update_unit(const UpdateArgs& a, int b, double n) {
   const int U = a.num_units;
   // The step counter lives on the device, so that a captured step replays
   // correctly: t = 1 + steps completed, the queue holds min(t - 1, delta)
@@ -165,7 +155,7 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   }
   // Counters and the list of C_t (integer atomics: exact; list order is
   // irrelevant to the selection).
-  if constexpr (L == 1) {
+  if constexpr (kWaveAgg) {
     const uint64_t active = __ballot(1);
     const int leader = __ffsll((unsigned long long)active) - 1;
     const int wl = threadIdx.x & 63;
@@ -191,6 +181,24 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
     if (tr) atomicAdd(&a.counters[kCntTrigR], 1);
     if (!finite) atomicAdd(&a.counters[kCntNonFinite], 1);
   }
+}
+
+// K2: L lanes per unit sum its partials; lane 0 then runs Alg. 1, the risk of
+// Alg. 2, and marks the unit's membership of the candidate pool C_t.
+template <int L>
+__global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
+  __shared__ double red[4];
+  const int lane = L == 1 ? 0 : int(threadIdx.x % L);
+  const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
+  if (b >= a.num_units) return;  // uniform per workgroup when L = 256
+  double n;
+  if (a.ext_norm != nullptr) {
+    n = a.ext_norm[b];
+  } else {
+    n = sqrt(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
+  }
+  if (lane != 0) return;
+  update_unit<L == 1>(a, b, n);
 }
 
 constexpr int kK3Block = 1024;
@@ -308,7 +316,7 @@ __device__ void bitonic_sort(int32_t* v) {
 // candidate with key > T is active, and the first `need` with key == T in
 // index order.  Pools of up to kK3Cap candidates are ranked in LDS; larger
 // ones over the global keys of all units.
-__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
+__device__ void select_body(const SelectArgs& a) {
   __shared__ uint64_t c_key[kK3Cap];
   __shared__ int32_t c_idx[kK3Cap];
   __shared__ int32_t tie_idx[kK3Block];
@@ -399,6 +407,8 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) {
     *a.step = t;
   }
 }
+
+__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) { select_body(a); }
 
 }  // namespace
 
