@@ -76,6 +76,75 @@ def cpu_baseline(torch, buf, lay, w, target_s: float = 12.0, max_units: int = 10
                       f"{w.bytes_per_step / 1e9:.2f} GB step"}
 
 
+def cpu_baseline_all_cores(buf, lay, w, single_gbs: float, target_s: float = 10.0,
+                           stage_bytes: float = 3e9):
+    """The same oracle norm pass spread over the host's cores, one thread per
+    core, each single-threaded inside NumPy (the oracle's float64 dot product
+    releases the GIL).  A fixed set of units, about stage_bytes in all, is
+    copied off the device once and swept repeatedly (copies not timed)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    from oracle import sumsq
+
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:                                  # pragma: no cover
+        limiter = None
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    order = np.random.default_rng(1).permutation(w.num_units)
+    staged, nbytes = [], 0
+    for b in order:
+        s = int(lay.seg_byte_off[b])
+        n = int(lay.seg_numel[b])
+        esz = 2 if int(lay.seg_dtype[b]) == 1 else 4
+        host = buf[s:s + n * esz].cpu().numpy()
+        staged.append(((host.view(np.uint16) if esz == 2 else host.view(np.float32)),
+                       int(lay.seg_dtype[b])))
+        nbytes += n * esz
+        if nbytes >= stage_bytes:
+            break
+    sweeps = max(1, int(round(single_gbs * 1e9 * cores * target_s / nbytes)))
+    tasks = staged * sweeps
+    with ThreadPoolExecutor(max_workers=cores) as pool:
+        t0 = time.perf_counter()
+        list(pool.map(lambda seg: sumsq([seg]), tasks))
+        spent = time.perf_counter() - t0
+    if limiter is not None:
+        limiter.unregister()
+    total = nbytes * sweeps
+    return {"value": round(total / spent / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"float64 NumPy oracle norm pass, {cores} threads over {len(staged)} "
+                      f"units ({nbytes / 1e9:.2f} GB) swept {sweeps} times "
+                      f"({total / 1e9:.1f} GB, {spent:.1f} s)"}
+
+
+def library_reduce_probe(torch, buf, lay, w, reps: int = 5):
+    """torch.linalg.vector_norm over the same gradient bytes viewed as one
+    flat tensor of the workload's dtype: the library's own read-reduce, as a
+    reference point for the gradient pass (a single-dtype workload only)."""
+    dts = {int(d) for d in lay.seg_dtype}
+    if len(dts) != 1:
+        return None
+    dt = torch.bfloat16 if dts.pop() == 1 else torch.float32
+    x = buf[:w.bytes_per_step].view(dt)
+    for _ in range(2):
+        torch.linalg.vector_norm(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        torch.linalg.vector_norm(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"kind": "torch.linalg.vector_norm over the same bytes", "ms": round(ms, 4),
+            "GBs": round(w.bytes_per_step / (ms * 1e-3) / 1e9, 1)}
+
+
 def measured_traffic(workload: str):
     """K1's HBM bytes per launch from the committed rocprofv3 counter summary,
     or None when it is for another workload or the kernel source has changed
@@ -169,6 +238,113 @@ def actuator_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     act.close()
 
 
+def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
+    """The controller step with its gradient pass fused into the producer:
+    the seven weight-gradient GEMMs of one LLaMA-2-13B layer (K5, the sum of
+    squares in the epilogue) followed by K2 + K3 from the tile partials,
+    against the unfused step: the same GEMMs by the vendor library
+    (torch.mm -> hipBLASLt) followed by gnmr_step (K1 re-reads every
+    gradient, then K2 + K3)."""
+    import numpy as np
+
+    from paper_2606_00539_amd import Controller, gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq
+    from synth import wgrad as SW
+
+    L = SW.llama2_13b_layer(tokens)
+    U = L.num_units
+    t0 = time.perf_counter()
+    dys, xs = [], []
+    for b, (o, i) in enumerate(L.shapes):
+        dy, x = SW.operands(L.seed, 1, b, tokens, o, i, dy_scale=L.dy_scale(1, b))
+        dys.append(torch.from_numpy(dy.view(np.int16)).to("cuda").view(torch.bfloat16))
+        xs.append(torch.from_numpy(x.view(np.int16)).to("cuda").view(torch.bfloat16))
+    log(f"[bench] wgrad operands generated in {time.perf_counter() - t0:.1f} s")
+    numel = [o * i for o, i in L.shapes]
+    off = np.concatenate([[0], np.cumsum(numel)]).astype(np.int64)
+    grads = torch.empty(int(off[-1]), dtype=torch.bfloat16, device="cuda")
+    dws = [grads[int(off[b]):int(off[b + 1])].view(o, i) for b, (o, i) in enumerate(L.shapes)]
+    tiles = [gnmr_wgrad_num_tiles(o, i) for o, i in L.shapes]
+    poff = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    parts = torch.empty(int(poff[-1]), dtype=torch.float32, device="cuda")
+    psl = [parts[int(poff[b]):int(poff[b + 1])] for b in range(U)]
+    ptrs = [d.data_ptr() for d in dws]
+    stream = torch.cuda.current_stream()
+    mk = lambda: Controller(U, 5, 2, 4, 1e-12, np.arange(U + 1), numel, [1] * U, ptrs,
+                            stream=stream)
+    fused, unfused = mk(), mk()
+    fused.bind_partials(poff)
+
+    def fused_step(t):
+        for b, (o, i) in enumerate(L.shapes):
+            gnmr_wgrad_sumsq(dys[b], xs[b], dws[b], tokens, o, i, psl[b], stream)
+        fused.step_from_partials(parts, 1.5 if t == 1 else 1.1, 1.5, stream)
+
+    def unfused_step(t):
+        for b in range(U):
+            torch.mm(dys[b].t(), xs[b], out=dws[b])
+        unfused.step(1.5 if t == 1 else 1.1, 1.5, stream=stream)
+
+    def gemms_only(kind):
+        for b, (o, i) in enumerate(L.shapes):
+            if kind == "k5":
+                gnmr_wgrad_sumsq(dys[b], xs[b], dws[b], tokens, o, i, psl[b], stream)
+            else:
+                torch.mm(dys[b].t(), xs[b], out=dws[b])
+
+    def timed(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for k in range(n):
+            fn(k + 1)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for k in range(warmup):
+        fused_step(k + 1)
+        unfused_step(k + 1)
+    torch.cuda.synchronize()
+    ms_fused = timed(fused_step, steps)
+    ms_unfused = timed(unfused_step, steps)
+    ms_k5 = timed(lambda _: gemms_only("k5"), steps)
+    ms_blas = timed(lambda _: gemms_only("blas"), steps)
+    # per-shape K5 and library GEMM times (the dominant kernel's roofline)
+    per_shape = {}
+    for b, (o, i) in enumerate(L.shapes[:1] + L.shapes[4:5] + L.shapes[6:7]):
+        bb = L.shapes.index((o, i))
+        f = 2.0 * tokens * o * i
+        k5 = timed(lambda _: gnmr_wgrad_sumsq(dys[bb], xs[bb], dws[bb], tokens, o, i, psl[bb],
+                                              stream), steps)
+        bl = timed(lambda _: torch.mm(dys[bb].t(), xs[bb], out=dws[bb]), steps)
+        per_shape[f"{o}x{i}"] = {"k5_ms": round(k5, 4), "k5_tflops": round(f / k5 / 1e9, 1),
+                                 "hipblaslt_ms": round(bl, 4),
+                                 "hipblaslt_tflops": round(f / bl / 1e9, 1)}
+    out = fused.query(stream=stream)
+    log(f"[bench] fused step stats {out['stats']}")
+    tflops = L.flops / (ms_k5 * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "GNMR step fused into the weight-gradient GEMMs, LLaMA-2-13B layer "
+                  "(GEMMs + controller step, TFLOP/s)",
+        "value": round(L.flops / (ms_fused * 1e-3) / 1e12, 1), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms_fused, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"LLaMA-2-13B decoder layer weight gradients, 7 units, "
+                               f"{tokens} tokens, bf16", "units": U, "tokens": tokens,
+                   "flops_per_step": L.flops, "grad_bytes": L.grad_bytes},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0,
+                     "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
+                     "kernel": "k5_wgrad", "kernel_ms_per_step": round(ms_k5, 4)},
+        "unfused": {"ms_per_step": round(ms_unfused, 4),
+                    "hipblaslt_gemms_ms": round(ms_blas, 4),
+                    "gnmr_step_ms": round(ms_unfused - ms_blas, 4)},
+        "fused_saving_ms": round(ms_unfused - ms_fused, 4),
+        "per_shape": per_shape}), flush=True)
+    fused.close()
+    unfused.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -182,6 +358,9 @@ def main():
     ap.add_argument("--actuator", action="store_true",
                     help="measure the recovery actuator (per-token fake quantisation of "
                          "LLaMA-2-7B-shaped saved activations) instead of the controller")
+    ap.add_argument("--wgrad", action="store_true",
+                    help="measure the gradient pass fused into the weight-gradient GEMMs of "
+                         "one LLaMA-2-13B layer against library GEMMs + gnmr_step")
     ap.add_argument("--tokens", type=int, default=4096)
     ap.add_argument("--probe-copy-bytes", type=float, default=0,
                     help="instead of the controller, time device-to-device copies of this "
@@ -207,6 +386,9 @@ def main():
         return
     if args.actuator:
         actuator_bench(torch, args.tokens, args.steps, args.warmup)
+        return
+    if args.wgrad:
+        wgrad_bench(torch, args.tokens, args.steps, args.warmup)
         return
     w = R.get(args.workload)
     lay = L.for_workload(w)
@@ -253,6 +435,18 @@ def main():
         log(f"[bench] {args.steps} graph replays in {elapsed:.6f} s")
     out = ctl.query(stream=stream)
     log(f"[bench] timed {args.steps} steps in {elapsed:.4f} s; stats {out['stats']}")
+    # the spread of single steps, each between a pair of events (after the timed region)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for e0, e1 in evs:
+        t += 1
+        e0.record(stream)
+        ctl.step(w.alpha(t), w.beta(t), stream=stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    step_us = np.array([e0.elapsed_time(e1) * 1e3 for e0, e1 in evs])
+    spread = {q: round(float(np.percentile(step_us, p)), 1)
+              for q, p in (("p10", 10), ("p50", 50), ("p90", 90))}
 
     ms = elapsed * 1e3 / args.steps
     gbs = w.bytes_per_step / (elapsed / args.steps) / 1e9
@@ -280,10 +474,17 @@ def main():
                    "launches_per_step": info["launches_per_step"],
                    "timing": "graph replays" if args.graph else "eager steps"},
         "roofline": roofline,
+        "step_us_spread": spread,
     }
+    probe = library_reduce_probe(torch, buf, lay, w)
+    if probe is not None:
+        result["library_reduce_probe"] = probe
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(torch, buf, lay, w)
+        log("[bench] timing the CPU oracle on all host cores")
+        result["cpu_baseline_all_cores"] = cpu_baseline_all_cores(
+            buf, lay, w, result["cpu_baseline"]["value"])
     ctl.close()
     print(json.dumps(result), flush=True)
 

@@ -148,6 +148,46 @@ gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm,
 gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
                        double* d_sumsq, void* stream);
 
+/* ---- producer-fused gradient pass (the norm from the weight-gradient GEMM) --
+ *
+ * The controller takes one number per unit from the gradient: its norm
+ * (Alg. 1; Sec. 3.3).  The producer of a linear layer's weight gradient
+ * holds every value of it in registers before writing it, so it can emit the
+ * sum of squares itself and the gradient pass (K1) never re-reads the
+ * gradient from HBM.
+ *
+ * gnmr_wgrad_sumsq: the weight-gradient GEMM of a linear layer y = x W^T,
+ *   dw[o][i] = bf16_rne( sum_t dy[t][o] * x[t][i] )     (fp32 accumulation)
+ * dy: device [tokens][out_features] bf16, x: device [tokens][in_features]
+ * bf16, dw: device [out_features][in_features] bf16, all row-major and
+ * 16-byte aligned; out_features and in_features multiples of 8; tokens >= 0
+ * (0 gives dw = 0).  tile_sumsq: device float [gnmr_wgrad_num_tiles(out,
+ * in)], written with the fp32 sum of float(dw)^2 over each 256x256 output
+ * tile (row-major tile order, ragged edge tiles included), each in a fixed
+ * order: deterministic.  The caller owns every buffer; dw must not overlap
+ * dy or x.  Asynchronous on `stream`.  GNMR_E_INVALID on a bad shape,
+ * pointer or alignment, GNMR_E_HIP on a launch failure. */
+int64_t gnmr_wgrad_num_tiles(int32_t out_features, int32_t in_features);
+gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t tokens,
+                             int32_t out_features, int32_t in_features,
+                             float* tile_sumsq, void* stream);
+
+/* Declare where a producer writes the units' partial sums of squares: unit b
+ * owns partials [unit_part_off[b], unit_part_off[b+1]) of a float array of
+ * num_partials (host array of num_units + 1, non-decreasing, [0] = 0, last =
+ * num_partials; copied).  Waits for the device; may be called again to
+ * re-bind.  GNMR_E_INVALID on a bad layout. */
+gnmr_status gnmr_bind_partials(gnmr_ctx* ctx, int64_t num_partials,
+                               const int64_t* unit_part_off);
+
+/* One controller step (K2 + K3) from the bound partials: n_b = sqrt of the
+ * float64 sum, in a fixed order, of unit b's partials in d_partial (device
+ * float [num_partials], e.g. the tile_sumsq of gnmr_wgrad_sumsq calls laid
+ * end to end), then Alg. 1 and Alg. 2 exactly as gnmr_step.  Asynchronous;
+ * capturable in a HIP graph.  GNMR_E_STATE if no layout is bound. */
+gnmr_status gnmr_step_from_partials(gnmr_ctx* ctx, const float* d_partial,
+                                    double alpha_t, double beta_t, void* stream);
+
 /* Copy the last step's outputs to host memory; every destination may be NULL.
  * Waits for `stream`.  Arrays are [num_units]: mask (1 = in A_t, recovery
  * path), lock (Lock_b after the step), norm (n_{b,t}), gnmr, dgnmr, risk (R).

@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libgnmr.so")
 SOURCES = [os.path.join(PKG, "csrc", f)
-           for f in ("gnmr_runtime.hip", "k1_sumsq.hip", "k23_control.hip", "k4_actuator.hip")]
+           for f in ("gnmr_runtime.hip", "k1_sumsq.hip", "k23_control.hip", "k4_actuator.hip",
+                     "k5_wgrad.hip")]
 HEADERS = [os.path.join(PKG, "csrc", f) for f in ("gnmr_internal.h", "k1_geometry.h")] + [
     os.path.join(ROOT, "include", "gnmr.h")]
 

@@ -27,7 +27,8 @@ EXPORTED = ("gnmr_init", "gnmr_destroy", "gnmr_step", "gnmr_step_from_norms", "g
             "gnmr_query", "gnmr_device_outputs", "gnmr_state_size", "gnmr_get_state",
             "gnmr_set_state", "gnmr_set_profiling", "gnmr_profile_read", "gnmr_info",
             "gnmr_last_error", "gnmr_actuator_create", "gnmr_actuate", "gnmr_actuator_info",
-            "gnmr_actuator_destroy")
+            "gnmr_actuator_destroy", "gnmr_wgrad_num_tiles", "gnmr_wgrad_sumsq",
+            "gnmr_bind_partials", "gnmr_step_from_partials")
 
 
 class GnmrError(RuntimeError):
@@ -95,11 +96,16 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "gnmr_actuate": [P, P, I32, I32, P],
         "gnmr_actuator_info": [P, P, P],
         "gnmr_actuator_destroy": [P],
+        "gnmr_wgrad_sumsq": [P, P, P, I64, I32, I32, P, P],
+        "gnmr_bind_partials": [P, I64, P],
+        "gnmr_step_from_partials": [P, P, D, D, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    lib.gnmr_wgrad_num_tiles.argtypes = [I32, I32]
+    lib.gnmr_wgrad_num_tiles.restype = I64
     lib.gnmr_last_error.argtypes = []
     lib.gnmr_last_error.restype = ctypes.c_char_p
     if path == _LIB_PATH:
@@ -168,6 +174,31 @@ def gnmr_sumsq(ctx, d_sumsq, seg_ptr=None, stream=None) -> None:
     p = d_sumsq.data_ptr() if hasattr(d_sumsq, "data_ptr") else int(d_sumsq)
     _check(load_library().gnmr_sumsq(ctx, None if ptrs is None else ctypes.cast(ptrs, ctypes.c_void_p),
                                      p, _stream(stream)))
+
+
+def _dptr(p) -> int:
+    return p.data_ptr() if hasattr(p, "data_ptr") else int(p)
+
+
+def gnmr_wgrad_num_tiles(out_features, in_features) -> int:
+    return int(load_library().gnmr_wgrad_num_tiles(int(out_features), int(in_features)))
+
+
+def gnmr_wgrad_sumsq(dy, x, dw, tokens, out_features, in_features, tile_sumsq,
+                     stream=None) -> None:
+    _check(load_library().gnmr_wgrad_sumsq(_dptr(dy), _dptr(x), _dptr(dw), int(tokens),
+                                           int(out_features), int(in_features),
+                                           _dptr(tile_sumsq), _stream(stream)))
+
+
+def gnmr_bind_partials(ctx, unit_part_off) -> None:
+    off = np.ascontiguousarray(unit_part_off, dtype=np.int64)
+    _check(load_library().gnmr_bind_partials(ctx, int(off[-1]), off.ctypes.data))
+
+
+def gnmr_step_from_partials(ctx, d_partial, alpha_t, beta_t, stream=None) -> None:
+    _check(load_library().gnmr_step_from_partials(ctx, _dptr(d_partial), float(alpha_t),
+                                                  float(beta_t), _stream(stream)))
 
 
 def gnmr_query(ctx, num_units, stream=None) -> dict:
@@ -310,6 +341,14 @@ class Controller:
 
     def sumsq(self, d_sumsq, seg_ptr=None, stream=None):
         gnmr_sumsq(self.ctx, d_sumsq, seg_ptr, stream)
+
+    def bind_partials(self, unit_part_off):
+        if len(unit_part_off) != self.num_units + 1:
+            raise ValueError(f"unit_part_off needs num_units + 1 = {self.num_units + 1} entries")
+        gnmr_bind_partials(self.ctx, unit_part_off)
+
+    def step_from_partials(self, d_partial, alpha_t, beta_t, stream=None):
+        gnmr_step_from_partials(self.ctx, d_partial, alpha_t, beta_t, stream)
 
     def query(self, stream=None) -> dict:
         return gnmr_query(self.ctx, self.num_units, stream)

@@ -93,6 +93,18 @@ struct RowItem {
   int32_t row;
 };
 
+// K5 (weight-gradient GEMM with the sum of squares in its epilogue):
+// 256x256 output tiles, K steps of 64, four waves; tiles walked in groups of
+// kWgGroupRows tile rows.
+constexpr int kWgBM = 256;
+constexpr int kWgBN = 256;
+constexpr int kWgBK = 64;
+constexpr int kWgThreads = 256;
+constexpr int kWgGroupRows = 8;
+
+int64_t wgrad_tiles(int32_t M, int32_t N);
+hipError_t launch_wgrad(const uint16_t* dy, const uint16_t* x, uint16_t* dw, int64_t K, int32_t M,
+                        int32_t N, float* tile_ss, hipStream_t s);
 hipError_t launch_actuate(const RowItem* items, int64_t num_rows, const ActSeg* segs,
                           const uint8_t* mask, int fmt_low, int fmt_rec, hipStream_t s);
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,

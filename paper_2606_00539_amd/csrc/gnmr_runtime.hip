@@ -101,6 +101,10 @@ struct gnmr_ctx {
   gnmr_stats* d_stats = nullptr;
   int64_t* d_step = nullptr;   // steps completed (advanced by K3)
 
+  // partial sums of squares made by a producer (gnmr_bind_partials)
+  int64_t* d_ext_off = nullptr;  // [U+1]
+  int64_t num_ext = -1;          // -1: none bound
+
   // pinned staging for segment-pointer uploads; `upload_done` guards reuse
   const void** h_ptr_stage = nullptr;
   hipEvent_t upload_done = nullptr;
@@ -166,8 +170,10 @@ gnmr_status record(gnmr_ctx* c, int which, hipStream_t st) {
   return GNMR_OK;
 }
 
-// K2 + K3 for step t+1 (K1 already enqueued when ext_norm is null).
-gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha, double beta,
+// K2 + K3 for step t+1 over the partial sums `partial` ([num_parts], unit b
+// owning [off[b], off[b+1])), or over the norms ext_norm when it is non-null.
+gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, const float* partial,
+                              const int64_t* off, int64_t num_parts, double alpha, double beta,
                               hipStream_t st) {
   gnmr::UpdateArgs u{};
   u.num_units = c->U;
@@ -180,8 +186,8 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   u.eps = c->eps;
   u.alpha = alpha;
   u.beta = beta;
-  u.unit_item_off = c->d_unit_item_off;
-  u.partial = c->d_partial;
+  u.unit_item_off = off;
+  u.partial = partial;
   u.ext_norm = ext_norm;
   u.A = c->d_A;
   u.Q = c->d_Q;
@@ -209,7 +215,7 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, double alpha,
   s.lock = c->d_lock;
   s.mask = c->d_mask;
   s.stats = c->d_stats;
-  GNMR_HIP(gnmr::launch_update(u, c->num_items, st));
+  GNMR_HIP(gnmr::launch_update(u, num_parts, st));
   gnmr_status r = record(c, 2, st);
   if (r != GNMR_OK) return r;
   GNMR_HIP(gnmr::launch_select(s, st));
@@ -227,6 +233,10 @@ void release(gnmr_ctx* c) {
       if (e) (void)hipEventDestroy(e);
   if (c->upload_done) (void)hipEventDestroy(c->upload_done);
   if (c->h_ptr_stage) (void)hipHostFree(c->h_ptr_stage);
+  if (c->d_ext_off) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(c->d_ext_off);
+  }
   if (c->arena) {
     (void)hipDeviceSynchronize();
     (void)hipFree(c->arena);
@@ -454,7 +464,8 @@ gnmr_status gnmr_step(gnmr_ctx* ctx, double alpha_t, double beta_t, const void* 
                               ctx->d_partial, st));
   r = record(ctx, 1, st);
   if (r != GNMR_OK) return r;
-  return update_and_select(ctx, nullptr, alpha_t, beta_t, st);
+  return update_and_select(ctx, nullptr, ctx->d_partial, ctx->d_unit_item_off, ctx->num_items,
+                           alpha_t, beta_t, st);
 }
 
 gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm, double alpha_t,
@@ -469,7 +480,72 @@ gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm, double alp
   r = record(ctx, 0, st);
   if (r == GNMR_OK) r = record(ctx, 1, st);
   if (r != GNMR_OK) return r;
-  return update_and_select(ctx, d_norm, alpha_t, beta_t, st);
+  return update_and_select(ctx, d_norm, ctx->d_partial, ctx->d_unit_item_off, ctx->num_items,
+                           alpha_t, beta_t, st);
+}
+
+gnmr_status gnmr_bind_partials(gnmr_ctx* ctx, int64_t num_partials,
+                               const int64_t* unit_part_off) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (unit_part_off == nullptr) return fail(GNMR_E_INVALID, "unit_part_off is NULL");
+  if (num_partials < 0) return fail(GNMR_E_INVALID, "num_partials must be >= 0");
+  if (unit_part_off[0] != 0 || unit_part_off[ctx->U] != num_partials)
+    return fail(GNMR_E_INVALID, "unit_part_off must start at 0 and end at num_partials");
+  for (int32_t b = 0; b < ctx->U; ++b)
+    if (unit_part_off[b + 1] < unit_part_off[b])
+      return fail(GNMR_E_INVALID, "unit_part_off must be non-decreasing");
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  const size_t bytes = size_t(ctx->U + 1) * sizeof(int64_t);
+  if (ctx->d_ext_off == nullptr) GNMR_HIP(hipMalloc(&ctx->d_ext_off, bytes));
+  GNMR_HIP(hipDeviceSynchronize());
+  GNMR_HIP(hipMemcpy(ctx->d_ext_off, unit_part_off, bytes, hipMemcpyHostToDevice));
+  ctx->num_ext = num_partials;
+  return GNMR_OK;
+}
+
+gnmr_status gnmr_step_from_partials(gnmr_ctx* ctx, const float* d_partial, double alpha_t,
+                                    double beta_t, void* stream) {
+  if (ctx == nullptr) return fail(GNMR_E_INVALID, "ctx is NULL");
+  if (ctx->num_ext < 0) return fail(GNMR_E_STATE, "no partial layout bound (gnmr_bind_partials)");
+  if (d_partial == nullptr && ctx->num_ext > 0) return fail(GNMR_E_INVALID, "d_partial is NULL");
+  gnmr_status r = check_thresholds(alpha_t, beta_t);
+  if (r != GNMR_OK) return r;
+  DeviceGuard g(ctx->device);
+  if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  r = record(ctx, 0, st);
+  if (r == GNMR_OK) r = record(ctx, 1, st);
+  if (r != GNMR_OK) return r;
+  return update_and_select(ctx, nullptr, d_partial, ctx->d_ext_off, ctx->num_ext, alpha_t, beta_t,
+                           st);
+}
+
+int64_t gnmr_wgrad_num_tiles(int32_t out_features, int32_t in_features) {
+  if (out_features <= 0 || in_features <= 0) return 0;
+  return gnmr::wgrad_tiles(out_features, in_features);
+}
+
+gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t tokens,
+                             int32_t out_features, int32_t in_features, float* tile_sumsq,
+                             void* stream) {
+  if (out_features <= 0 || in_features <= 0 || tokens < 0)
+    return fail(GNMR_E_INVALID, "out_features and in_features must be > 0, tokens >= 0");
+  if (out_features % 8 != 0 || in_features % 8 != 0)
+    return fail(GNMR_E_INVALID, "out_features and in_features must be multiples of 8");
+  if (out_features > (1 << 24) || in_features > (1 << 24))
+    return fail(GNMR_E_INVALID, "out_features and in_features must be <= 2^24");
+  if (dw == nullptr || tile_sumsq == nullptr || (tokens > 0 && (dy == nullptr || x == nullptr)))
+    return fail(GNMR_E_INVALID, "dy, x, dw and tile_sumsq must be device pointers");
+  if ((reinterpret_cast<uintptr_t>(dy) | reinterpret_cast<uintptr_t>(x) |
+       reinterpret_cast<uintptr_t>(dw)) % 16 != 0)
+    return fail(GNMR_E_INVALID, "dy, x and dw must be 16-byte aligned");
+  if (gnmr::wgrad_tiles(out_features, in_features) > int64_t(INT32_MAX))
+    return fail(GNMR_E_INVALID, "too many output tiles");
+  GNMR_HIP(gnmr::launch_wgrad(static_cast<const uint16_t*>(dy), static_cast<const uint16_t*>(x),
+                              static_cast<uint16_t*>(dw), tokens, out_features, in_features,
+                              tile_sumsq, static_cast<hipStream_t>(stream)));
+  return GNMR_OK;
 }
 
 gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr, double* d_sumsq,

@@ -99,3 +99,28 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "8"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+@pytest.mark.parametrize("bad", [
+    dict(out_f=12), dict(in_f=4), dict(out_f=0), dict(in_f=-8), dict(tokens=-1),
+    dict(dy=0), dict(x=0), dict(dw=0), dict(ss=0), dict(dy=4096 + 8), dict(dw=8192 + 2),
+])
+def test_wgrad_rejects_bad_arguments(bad):
+    # every case fails in the argument checks, before any device call
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    a = dict(dy=4096, x=8192, dw=16384, tokens=16, out_f=64, in_f=128, ss=32768)
+    a.update(bad)
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_wgrad_sumsq(a["dy"], a["x"], a["dw"], a["tokens"], a["out_f"], a["in_f"], a["ss"])
+    assert e.value.status == B.GNMR_E_INVALID
+
+
+def test_wgrad_tile_count():
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles
+
+    assert gnmr_wgrad_num_tiles(5120, 5120) == 400
+    assert gnmr_wgrad_num_tiles(13824, 5120) == 54 * 20
+    assert gnmr_wgrad_num_tiles(264, 520) == 2 * 3
+    assert gnmr_wgrad_num_tiles(0, 8) == 0

@@ -1,0 +1,219 @@
+"""Parity of the producer-fused gradient pass: the weight-gradient GEMM with
+the sum of squares in its epilogue (gnmr_wgrad_sumsq), and the controller
+step fed by its tile partials (gnmr_step_from_partials).
+
+Bars (oracle/wgrad.py states the readings):
+  * integer operands whose every partial sum is exact in fp32 and bf16: dw
+    bit-exact against the oracle, over several tiles and ragged edges in all
+    three dimensions;
+  * random bf16 operands: every dw element within error_bound() of the
+    float64 product, and each tile's sum of squares equal to the float64 sum
+    of squares of the dw values the kernel stored, within the fp32
+    summation bound (264 additions of non-negative terms: 264 * 2^-24);
+  * full size (13B layer shapes, 4096 tokens): sampled dw elements, computed
+    one by one by the oracle, and sampled tiles;
+  * controller: masks, locks and counters bit-exact against the oracle
+    controller fed with the oracle's norms, and against gnmr_step (K1) over
+    the same stored gradients.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from gpu_util import assert_step_matches, require_gpu
+from oracle import Controller as Oracle
+from oracle import wgrad as W
+from synth import wgrad as SW
+
+pytestmark = pytest.mark.gpu
+
+SS_RTOL = 264 * 2.0 ** -24
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(torch, bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda")
+
+
+def run_wgrad(torch, dy_bits, x_bits, dw=None, ss=None):
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq
+
+    T, M = dy_bits.shape
+    N = x_bits.shape[1]
+    d_dy, d_x = to_dev(torch, dy_bits), to_dev(torch, x_bits)
+    if dw is None:
+        dw = torch.full((M, N), 0x5555, dtype=torch.int16, device="cuda")   # unwritten marker
+    nt = gnmr_wgrad_num_tiles(M, N)
+    if ss is None:
+        ss = torch.full((nt,), float("nan"), dtype=torch.float32, device="cuda")
+    gnmr_wgrad_sumsq(d_dy, d_x, dw, T, M, N, ss)
+    torch.cuda.synchronize()
+    return dw.cpu().numpy().view(np.uint16), ss.cpu().numpy()
+
+
+@pytest.mark.parametrize("M,N,T", [(256, 256, 64), (264, 520, 70), (520, 776, 130),
+                                   (8, 8, 1), (16, 2056, 33), (1032, 264, 200)])
+def test_integer_operands_bit_exact(M, N, T):
+    torch = require_gpu()
+    say(f"wgrad integer M={M} N={N} T={T}")
+    dy, x = SW.small_integer_operands(M * 7 + N + T, T, M, N, vmax=1)
+    dw, ss = run_wgrad(torch, dy, x)
+    exact = W.wgrad_exact(dy, x)
+    want = W.bf16_rne(exact)
+    bad = np.argwhere(dw != want)
+    assert bad.size == 0, f"dw differs at {bad[:8].tolist()}"
+    ref = W.tile_sumsq(want)
+    assert ss.shape == ref.shape
+    np.testing.assert_allclose(ss, ref, rtol=SS_RTOL, atol=0)
+
+
+def test_empty_batch_gives_zero_gradient():
+    torch = require_gpu()
+    dy = np.zeros((0, 264), np.uint16)
+    x = np.zeros((0, 520), np.uint16)
+    dw, ss = run_wgrad(torch, dy, x)
+    assert np.all(dw == 0) and np.all(ss == 0.0)
+
+
+def test_single_token_outer_product():
+    torch = require_gpu()
+    dy, x = SW.operands(5, 1, 0, tokens=1, out_f=272, in_f=328)
+    dw, _ = run_wgrad(torch, dy, x)
+    # one product per element: exact in fp32, so one rounding to bf16
+    assert np.array_equal(dw, W.bf16_rne(W.wgrad_exact(dy, x)))
+
+
+@pytest.mark.parametrize("M,N,T", [(576, 776, 1000), (256, 512, 4096), (200, 264, 65)])
+def test_random_operands_within_bound(M, N, T):
+    torch = require_gpu()
+    say(f"wgrad random M={M} N={N} T={T}")
+    dy, x = SW.operands(1, 1, M + N, tokens=T, out_f=M, in_f=N)
+    dw, ss = run_wgrad(torch, dy, x)
+    exact = W.wgrad_exact(dy, x)
+    bound = W.error_bound(dy, x, exact)
+    err = np.abs(W.widen_bf16(dw) - exact)
+    bad = np.argwhere(err > bound)
+    assert bad.size == 0, f"dw outside the bound at {bad[:8].tolist()}"
+    # the epilogue sums the squares of exactly what it stored
+    np.testing.assert_allclose(ss, W.tile_sumsq(dw), rtol=SS_RTOL, atol=0)
+    # and the unit norm is within the bound's reach of the oracle's
+    # (triangle inequality: | ||q|| - ||r|| | <= ||q - r|| <= ||2 bound||)
+    n_gpu = np.sqrt(np.sum(ss.astype(np.float64)))
+    n_ref = W.unit_norm(W.bf16_rne(exact))
+    assert abs(n_gpu - n_ref) <= 2 * np.sqrt(np.sum(bound * bound)) + SS_RTOL * n_ref
+
+
+def test_output_buffer_fully_written_and_nothing_else():
+    torch = require_gpu()
+    M, N, T = 264, 520, 70
+    dy, x = SW.operands(2, 1, 9, tokens=T, out_f=M, in_f=N)
+    guard = torch.full((M * N + 4096,), 0x5555, dtype=torch.int16, device="cuda")
+    dw_view = guard[:M * N].view(M, N)
+    run_wgrad(torch, dy, x, dw=dw_view)
+    tail = guard[M * N:].cpu().numpy()
+    assert np.all(tail == 0x5555), "K5 wrote past the end of dw"
+    assert not np.any(dw_view.cpu().numpy().view(np.uint16) == 0x5555)
+
+
+@pytest.mark.parametrize("M,N", [(13824, 5120), (5120, 13824)])
+def test_fullsize_sampled(M, N):
+    torch = require_gpu()
+    T = 4096
+    say(f"wgrad full size M={M} N={N} T={T}")
+    dy, x = SW.operands(0, 1, 4, tokens=T, out_f=M, in_f=N)
+    dw, ss = run_wgrad(torch, dy, x)
+    assert ss.size == W.num_tiles(M, N)
+    rng = np.random.default_rng(M)
+    rows = rng.choice(M, 24, replace=False)
+    cols = rng.choice(N, 24, replace=False)
+    exact = W.wgrad_exact(dy[:, rows], x[:, cols])
+    bound = W.error_bound(dy[:, rows], x[:, cols], exact)
+    err = np.abs(W.widen_bf16(dw[np.ix_(rows, cols)]) - exact)
+    assert np.all(err <= bound)
+    tn = -(-N // 256)
+    for tile in rng.choice(ss.size, 4, replace=False):
+        a, b = divmod(int(tile), tn)
+        blk = dw[a * 256:(a + 1) * 256, b * 256:(b + 1) * 256]
+        np.testing.assert_allclose(ss[tile], W.tile_sumsq(blk)[0], rtol=SS_RTOL, atol=0)
+
+
+def small_layer():
+    return SW.WgradLayer("small-layer", ((512, 512), (512, 512), (512, 512), (512, 512),
+                                         (1376, 512), (1376, 512), (512, 1376)), tokens=256)
+
+
+def test_controller_from_partials_matches_oracle_and_k1():
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller, gnmr_wgrad_num_tiles
+
+    L = small_layer()
+    U = L.num_units
+    steps, window, max_o, lock_len, eps = 14, 5, 2, 3, 1e-12
+    numel = [o * i for o, i in L.shapes]
+    off = np.concatenate([[0], np.cumsum(numel)]).astype(np.int64)
+    grads = torch.zeros(int(off[-1]), dtype=torch.int16, device="cuda")
+    tiles = [gnmr_wgrad_num_tiles(o, i) for o, i in L.shapes]
+    part_off = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    parts = torch.zeros(int(part_off[-1]), dtype=torch.float32, device="cuda")
+    ptrs = [grads.data_ptr() + 2 * int(off[b]) for b in range(U)]
+    fused = Controller(U, window, max_o, lock_len, eps, np.arange(U + 1), numel, [1] * U, ptrs)
+    fused.bind_partials(part_off)
+    k1 = Controller(U, window, max_o, lock_len, eps, np.arange(U + 1), numel, [1] * U, ptrs)
+    ora = Oracle(U, window=window, max_o=max_o, lock_len=lock_len, eps=eps)
+    from paper_2606_00539_amd import gnmr_wgrad_sumsq
+    try:
+        for t in range(1, steps + 1):
+            alpha, beta = (1.5 if t == 1 else 1.1), 1.5
+            norms = np.zeros(U)
+            for b, (o, i) in enumerate(L.shapes):
+                dy, x = SW.operands(L.seed, t, b, L.tokens, o, i, dy_scale=L.dy_scale(t, b))
+                d_dy, d_x = to_dev(torch, dy), to_dev(torch, x)
+                dw = grads[int(off[b]):int(off[b + 1])]
+                gnmr_wgrad_sumsq(d_dy, d_x, dw, L.tokens, o, i,
+                                 parts[int(part_off[b]):int(part_off[b + 1])])
+                norms[b] = W.unit_norm(W.bf16_rne(W.wgrad_exact(dy, x)))
+            fused.step_from_partials(parts, alpha, beta)
+            k1.step(alpha, beta)
+            ref = ora.step(norms, alpha, beta)
+            # the scenario keeps every decision clear of its threshold
+            g, d = ref.gnmr / alpha, ref.dgnmr / beta
+            assert np.all(np.abs(g - 1) > 1e-3) and np.all(np.abs(d - 1) > 1e-3), f"t={t}"
+            out_f, out_k = fused.query(), k1.query()
+            # bf16 rounding of the fp32 accumulation moves a norm by far less
+            # than 1e-3 relative; decisions must agree exactly
+            assert_step_matches(out_f, ref, rtol=1e-3, what=f"fused t={t}")
+            assert_step_matches(out_k, ref, rtol=1e-3, what=f"k1 t={t}")
+            np.testing.assert_allclose(out_f["norm"], out_k["norm"], rtol=1e-5, atol=0,
+                                       err_msg=f"t={t}: fused vs K1 norms of the same gradient")
+            say(f"  t={t} ok: {out_f['stats']}")
+        assert out_f["stats"]["t"] == steps
+    finally:
+        fused.close()
+        k1.close()
+
+
+def test_partials_binding_errors():
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller, GnmrError
+
+    with Controller(3, 5, 1, 2, 0.0, [0, 1, 2, 3], [8, 8, 8], [1, 1, 1]) as ctl:
+        parts = torch.zeros(4, dtype=torch.float32, device="cuda")
+        with pytest.raises(GnmrError, match="GNMR_E_STATE"):
+            ctl.step_from_partials(parts, 1.5, 1.5)
+        for bad in ([1, 1, 2, 4], [0, 3, 2, 4], [0, 1, 2, -1]):
+            with pytest.raises(GnmrError, match="GNMR_E_INVALID"):
+                ctl.bind_partials(bad)
+        with pytest.raises(ValueError):
+            ctl.bind_partials([0, 1, 4])
+        ctl.bind_partials([0, 1, 3, 4])
+        with pytest.raises(GnmrError, match="GNMR_E_INVALID"):
+            ctl.step_from_partials(parts, -1.0, 1.5)
+        parts.copy_(torch.tensor([4.0, 1.0, 3.0, 9.0]))
+        ctl.step_from_partials(parts, 1.5, 1.5)
+        out = ctl.query()
+        np.testing.assert_allclose(out["norm"], [2.0, 2.0, 3.0], rtol=1e-15)
