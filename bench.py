@@ -247,7 +247,8 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     gradient, then K2 + K3)."""
     import numpy as np
 
-    from paper_2606_00539_amd import Controller, gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq
+    from paper_2606_00539_amd import (Controller, gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq,
+                                      gnmr_wgrad_sumsq_batched)
     from synth import wgrad as SW
 
     L = SW.llama2_13b_layer(tokens)
@@ -274,9 +275,10 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     fused, unfused = mk(), mk()
     fused.bind_partials(poff)
 
+    problems = [(dys[b], xs[b], dws[b], tokens, o, i) for b, (o, i) in enumerate(L.shapes)]
+
     def fused_step(t):
-        for b, (o, i) in enumerate(L.shapes):
-            gnmr_wgrad_sumsq(dys[b], xs[b], dws[b], tokens, o, i, psl[b], stream)
+        gnmr_wgrad_sumsq_batched(problems, parts, stream)
         fused.step_from_partials(parts, 1.5 if t == 1 else 1.1, 1.5, stream)
 
     def unfused_step(t):
@@ -287,7 +289,8 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     def gemms_only(kind):
         for b, (o, i) in enumerate(L.shapes):
             if kind == "k5":
-                gnmr_wgrad_sumsq(dys[b], xs[b], dws[b], tokens, o, i, psl[b], stream)
+                gnmr_wgrad_sumsq_batched(problems, parts, stream)
+                break
             else:
                 torch.mm(dys[b].t(), xs[b], out=dws[b])
 

@@ -172,6 +172,25 @@ gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t to
                              int32_t out_features, int32_t in_features,
                              float* tile_sumsq, void* stream);
 
+/* Several weight-gradient GEMMs (e.g. the seven projections of a decoder
+ * layer) in one launch, so that their tiles share the machine: each problem
+ * as in gnmr_wgrad_sumsq; problem i's tile sums start at tile_sumsq + the
+ * tile counts of problems 0..i-1 (the layout gnmr_bind_partials expects with
+ * one unit per problem).  `problems` is a host array, read before return;
+ * every check of gnmr_wgrad_sumsq applies to each problem, and nothing is
+ * launched if one fails. */
+typedef struct {
+  const void* dy;        /* device [tokens][out_features] bf16 */
+  const void* x;         /* device [tokens][in_features] bf16  */
+  void* dw;              /* device [out_features][in_features] bf16 */
+  int64_t tokens;
+  int32_t out_features;
+  int32_t in_features;
+} gnmr_wgrad_problem;
+gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems,
+                                     int32_t num_problems, float* tile_sumsq,
+                                     void* stream);
+
 /* Declare where a producer writes the units' partial sums of squares: unit b
  * owns partials [unit_part_off[b], unit_part_off[b+1]) of a float array of
  * num_partials (host array of num_units + 1, non-decreasing, [0] = 0, last =

@@ -28,7 +28,7 @@ EXPORTED = ("gnmr_init", "gnmr_destroy", "gnmr_step", "gnmr_step_from_norms", "g
             "gnmr_set_state", "gnmr_set_profiling", "gnmr_profile_read", "gnmr_info",
             "gnmr_last_error", "gnmr_actuator_create", "gnmr_actuate", "gnmr_actuator_info",
             "gnmr_actuator_destroy", "gnmr_wgrad_num_tiles", "gnmr_wgrad_sumsq",
-            "gnmr_bind_partials", "gnmr_step_from_partials")
+            "gnmr_bind_partials", "gnmr_step_from_partials", "gnmr_wgrad_sumsq_batched")
 
 
 class GnmrError(RuntimeError):
@@ -53,6 +53,12 @@ class gnmr_segments(ctypes.Structure):
 class gnmr_act_segment(ctypes.Structure):
     _fields_ = [("in_", ctypes.c_void_p), ("out", ctypes.c_void_p), ("rows", ctypes.c_int64),
                 ("cols", ctypes.c_int32), ("unit", ctypes.c_int32)]
+
+
+class gnmr_wgrad_problem(ctypes.Structure):
+    _fields_ = [("dy", ctypes.c_void_p), ("x", ctypes.c_void_p), ("dw", ctypes.c_void_p),
+                ("tokens", ctypes.c_int64), ("out_features", ctypes.c_int32),
+                ("in_features", ctypes.c_int32)]
 
 
 class gnmr_stats(ctypes.Structure):
@@ -98,6 +104,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "gnmr_actuator_destroy": [P],
         "gnmr_wgrad_sumsq": [P, P, P, I64, I32, I32, P, P],
         "gnmr_bind_partials": [P, I64, P],
+        "gnmr_wgrad_sumsq_batched": [P, I32, P, P],
         "gnmr_step_from_partials": [P, P, D, D, P],
     }
     for name, args in sig.items():
@@ -189,6 +196,15 @@ def gnmr_wgrad_sumsq(dy, x, dw, tokens, out_features, in_features, tile_sumsq,
     _check(load_library().gnmr_wgrad_sumsq(_dptr(dy), _dptr(x), _dptr(dw), int(tokens),
                                            int(out_features), int(in_features),
                                            _dptr(tile_sumsq), _stream(stream)))
+
+
+def gnmr_wgrad_sumsq_batched(problems, tile_sumsq, stream=None) -> None:
+    """problems: iterable of (dy, x, dw, tokens, out_features, in_features)."""
+    ps = [gnmr_wgrad_problem(_dptr(a), _dptr(b), _dptr(c), int(t), int(o), int(i))
+          for a, b, c, t, o, i in problems]
+    arr = (gnmr_wgrad_problem * max(len(ps), 1))(*ps)
+    _check(load_library().gnmr_wgrad_sumsq_batched(arr, len(ps), _dptr(tile_sumsq),
+                                                   _stream(stream)))
 
 
 def gnmr_bind_partials(ctx, unit_part_off) -> None:

@@ -102,9 +102,27 @@ constexpr int kWgBK = 64;
 constexpr int kWgThreads = 256;
 constexpr int kWgGroupRows = 8;
 
+constexpr int kWgMaxBatch = 16;   // problems per launch (passed by value)
+
+struct WgProblem {
+  const uint16_t* dy;  // [K][M]
+  const uint16_t* x;   // [K][N]
+  uint16_t* dw;        // [M][N]
+  float* tile_ss;      // [tiles_m * tiles_n]
+  int64_t K;
+  int32_t M, N, tiles_m, tiles_n;
+  int32_t tile_begin;  // first tile of this problem in the launch's tile order
+  int32_t pad;
+};
+
+struct WgBatch {
+  int32_t num;
+  int32_t total_tiles;
+  WgProblem p[kWgMaxBatch];
+};
+
 int64_t wgrad_tiles(int32_t M, int32_t N);
-hipError_t launch_wgrad(const uint16_t* dy, const uint16_t* x, uint16_t* dw, int64_t K, int32_t M,
-                        int32_t N, float* tile_ss, hipStream_t s);
+hipError_t launch_wgrad(const WgBatch& batch, hipStream_t s);
 hipError_t launch_actuate(const RowItem* items, int64_t num_rows, const ActSeg* segs,
                           const uint8_t* mask, int fmt_low, int fmt_rec, hipStream_t s);
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,

@@ -526,26 +526,64 @@ int64_t gnmr_wgrad_num_tiles(int32_t out_features, int32_t in_features) {
   return gnmr::wgrad_tiles(out_features, in_features);
 }
 
+gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t num_problems,
+                                     float* tile_sumsq, void* stream) {
+  if (num_problems < 0 || (num_problems > 0 && problems == nullptr))
+    return fail(GNMR_E_INVALID, "problems must hold num_problems >= 0 entries");
+  if (num_problems > 0 && tile_sumsq == nullptr)
+    return fail(GNMR_E_INVALID, "tile_sumsq must be a device pointer");
+  for (int32_t i = 0; i < num_problems; ++i) {
+    const gnmr_wgrad_problem& q = problems[i];
+    if (q.out_features <= 0 || q.in_features <= 0 || q.tokens < 0)
+      return fail(GNMR_E_INVALID, "out_features and in_features must be > 0, tokens >= 0");
+    if (q.out_features % 8 != 0 || q.in_features % 8 != 0)
+      return fail(GNMR_E_INVALID, "out_features and in_features must be multiples of 8");
+    if (q.out_features > (1 << 24) || q.in_features > (1 << 24))
+      return fail(GNMR_E_INVALID, "out_features and in_features must be <= 2^24");
+    if (q.dw == nullptr || (q.tokens > 0 && (q.dy == nullptr || q.x == nullptr)))
+      return fail(GNMR_E_INVALID, "dy, x and dw must be device pointers");
+    if ((reinterpret_cast<uintptr_t>(q.dy) | reinterpret_cast<uintptr_t>(q.x) |
+         reinterpret_cast<uintptr_t>(q.dw)) % 16 != 0)
+      return fail(GNMR_E_INVALID, "dy, x and dw must be 16-byte aligned");
+    if (gnmr::wgrad_tiles(q.out_features, q.in_features) > int64_t(INT32_MAX / 2))
+      return fail(GNMR_E_INVALID, "too many output tiles");
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int64_t base = 0;  // first partial of the current launch
+  for (int32_t i = 0; i < num_problems;) {
+    gnmr::WgBatch b{};
+    int64_t tiles = 0;
+    while (i < num_problems && b.num < gnmr::kWgMaxBatch) {
+      const gnmr_wgrad_problem& q = problems[i];
+      const int64_t t = gnmr::wgrad_tiles(q.out_features, q.in_features);
+      if (b.num > 0 && tiles + t > int64_t(INT32_MAX / 2)) break;
+      gnmr::WgProblem& P = b.p[b.num++];
+      P.dy = static_cast<const uint16_t*>(q.dy);
+      P.x = static_cast<const uint16_t*>(q.x);
+      P.dw = static_cast<uint16_t*>(q.dw);
+      P.tile_ss = tile_sumsq + base + tiles;
+      P.K = q.tokens;
+      P.M = q.out_features;
+      P.N = q.in_features;
+      P.tiles_m = (q.out_features + gnmr::kWgBM - 1) / gnmr::kWgBM;
+      P.tiles_n = (q.in_features + gnmr::kWgBN - 1) / gnmr::kWgBN;
+      P.tile_begin = int32_t(tiles);
+      tiles += t;
+      ++i;
+    }
+    b.total_tiles = int32_t(tiles);
+    GNMR_HIP(gnmr::launch_wgrad(b, st));
+    base += tiles;
+  }
+  return GNMR_OK;
+}
+
 gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t tokens,
                              int32_t out_features, int32_t in_features, float* tile_sumsq,
                              void* stream) {
-  if (out_features <= 0 || in_features <= 0 || tokens < 0)
-    return fail(GNMR_E_INVALID, "out_features and in_features must be > 0, tokens >= 0");
-  if (out_features % 8 != 0 || in_features % 8 != 0)
-    return fail(GNMR_E_INVALID, "out_features and in_features must be multiples of 8");
-  if (out_features > (1 << 24) || in_features > (1 << 24))
-    return fail(GNMR_E_INVALID, "out_features and in_features must be <= 2^24");
-  if (dw == nullptr || tile_sumsq == nullptr || (tokens > 0 && (dy == nullptr || x == nullptr)))
-    return fail(GNMR_E_INVALID, "dy, x, dw and tile_sumsq must be device pointers");
-  if ((reinterpret_cast<uintptr_t>(dy) | reinterpret_cast<uintptr_t>(x) |
-       reinterpret_cast<uintptr_t>(dw)) % 16 != 0)
-    return fail(GNMR_E_INVALID, "dy, x and dw must be 16-byte aligned");
-  if (gnmr::wgrad_tiles(out_features, in_features) > int64_t(INT32_MAX))
-    return fail(GNMR_E_INVALID, "too many output tiles");
-  GNMR_HIP(gnmr::launch_wgrad(static_cast<const uint16_t*>(dy), static_cast<const uint16_t*>(x),
-                              static_cast<uint16_t*>(dw), tokens, out_features, in_features,
-                              tile_sumsq, static_cast<hipStream_t>(stream)));
-  return GNMR_OK;
+  if (tile_sumsq == nullptr) return fail(GNMR_E_INVALID, "tile_sumsq must be a device pointer");
+  const gnmr_wgrad_problem q{dy, x, dw, tokens, out_features, in_features};
+  return gnmr_wgrad_sumsq_batched(&q, 1, tile_sumsq, stream);
 }
 
 gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr, double* d_sumsq,

@@ -57,22 +57,28 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* p0, const uint16_t* p1) {
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-__global__ __launch_bounds__(kWgThreads) void k5_wgrad(const uint16_t* __restrict__ dy,
-                                                       const uint16_t* __restrict__ x,
-                                                       uint16_t* __restrict__ dw, int64_t K,
-                                                       int M, int N, int tiles_m, int tiles_n,
-                                                       float* __restrict__ tile_ss) {
+__global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kStage];  // [stage][x, dy]
   __shared__ float red[kWgThreads / 64];
 
   // Workgroup -> tile: workgroups w, w+8, ... run on one XCD, so give each
-  // XCD a contiguous run of the tile order; the order walks groups of 8
-  // tile rows column by column, so that the tiles an XCD holds at once share
-  // their dy and x panels in its L2.
-  const int G = tiles_m * tiles_n;
+  // XCD a contiguous run of the tile order (over all problems of the batch);
+  // inside a problem the order walks groups of 8 tile rows column by column,
+  // so that the tiles an XCD holds at once share their dy and x panels in
+  // its L2.
+  const int G = batch.total_tiles;
   const int w = blockIdx.x;
   const int xcd = w % kNumXcd, q = G / kNumXcd, r = G % kNumXcd;
-  const int v = xcd * q + (xcd < r ? xcd : r) + w / kNumXcd;
+  int v = xcd * q + (xcd < r ? xcd : r) + w / kNumXcd;
+  int pi = 0;
+  while (pi + 1 < batch.num && v >= batch.p[pi + 1].tile_begin) ++pi;
+  const WgProblem& P = batch.p[pi];
+  v -= P.tile_begin;
+  const uint16_t* __restrict__ dy = P.dy;
+  const uint16_t* __restrict__ x = P.x;
+  uint16_t* __restrict__ dw = P.dw;
+  const int64_t K = P.K;
+  const int M = P.M, N = P.N, tiles_m = P.tiles_m, tiles_n = P.tiles_n;
   const int per_group = kWgGroupRows * tiles_n;
   const int first_m = (v / per_group) * kWgGroupRows;
   const int rows = tiles_m - first_m < kWgGroupRows ? tiles_m - first_m : kWgGroupRows;
@@ -194,7 +200,7 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const uint16_t* __restric
   for (int d = 32; d >= 1; d >>= 1) ss += __shfl_xor(ss, d, 64);
   if (lane == 0) red[wave] = ss;
   __syncthreads();
-  if (tid == 0) tile_ss[tm * tiles_n + tn] = ((red[0] + red[1]) + red[2]) + red[3];
+  if (tid == 0) P.tile_ss[tm * tiles_n + tn] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
 }  // namespace
@@ -203,12 +209,9 @@ int64_t wgrad_tiles(int32_t M, int32_t N) {
   return int64_t((M + kWgBM - 1) / kWgBM) * int64_t((N + kWgBN - 1) / kWgBN);
 }
 
-hipError_t launch_wgrad(const uint16_t* dy, const uint16_t* x, uint16_t* dw, int64_t K, int32_t M,
-                        int32_t N, float* tile_ss, hipStream_t s) {
-  const int tiles_m = (M + kWgBM - 1) / kWgBM, tiles_n = (N + kWgBN - 1) / kWgBN;
-  if (tiles_m == 0 || tiles_n == 0) return hipSuccess;
-  hipLaunchKernelGGL(k5_wgrad, dim3(unsigned(tiles_m * tiles_n)), dim3(kWgThreads), 0, s, dy, x,
-                     dw, K, M, N, tiles_m, tiles_n, tile_ss);
+hipError_t launch_wgrad(const WgBatch& batch, hipStream_t s) {
+  if (batch.total_tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(k5_wgrad, dim3(unsigned(batch.total_tiles)), dim3(kWgThreads), 0, s, batch);
   return hipGetLastError();
 }
 

@@ -40,6 +40,7 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(B.gnmr_config) == 40
     assert ctypes.sizeof(B.gnmr_segments) == 40
     assert ctypes.sizeof(B.gnmr_stats) == 40
+    assert ctypes.sizeof(B.gnmr_wgrad_problem) == 40
 
 
 @pytest.mark.parametrize("bad", [
@@ -124,3 +125,16 @@ def test_wgrad_tile_count():
     assert gnmr_wgrad_num_tiles(13824, 5120) == 54 * 20
     assert gnmr_wgrad_num_tiles(264, 520) == 2 * 3
     assert gnmr_wgrad_num_tiles(0, 8) == 0
+
+
+def test_wgrad_batched_rejects_a_bad_problem_before_launching():
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    good = (4096, 8192, 16384, 16, 64, 128)
+    bad = (4096, 8192, 16384, 16, 60, 128)
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_wgrad_sumsq_batched([good, bad], 32768)
+    assert e.value.status == B.GNMR_E_INVALID
+    with pytest.raises(GnmrError):
+        B.gnmr_wgrad_sumsq_batched([good], 0)

@@ -142,6 +142,38 @@ def test_fullsize_sampled(M, N):
         np.testing.assert_allclose(ss[tile], W.tile_sumsq(blk)[0], rtol=SS_RTOL, atol=0)
 
 
+@pytest.mark.parametrize("count", [5, 20])
+def test_batched_matches_single_problem_calls(count):
+    """One launch over several problems (and more than one launch past 16
+    problems): every dw bit-identical to the oracle on integer operands and
+    to the single-problem entry, tile sums at the concatenated offsets."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    shapes = [(264, 520, 70), (8, 8, 1), (1032, 264, 200), (16, 2056, 33), (512, 256, 0)]
+    shapes = [shapes[i % len(shapes)] for i in range(count)]
+    say(f"wgrad batched, {count} problems")
+    ops = [SW.small_integer_operands(11 + i, T, M, N) for i, (M, N, T) in enumerate(shapes)]
+    dev = [(to_dev(torch, dy), to_dev(torch, x),
+            torch.full((M, N), 0x5555, dtype=torch.int16, device="cuda"))
+           for (dy, x), (M, N, T) in zip(ops, shapes)]
+    tiles = [gnmr_wgrad_num_tiles(M, N) for M, N, _ in shapes]
+    off = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    ss = torch.full((int(off[-1]),), float("nan"), dtype=torch.float32, device="cuda")
+    gnmr_wgrad_sumsq_batched([(a, b, c, T, M, N) for (a, b, c), (M, N, T) in zip(dev, shapes)],
+                             ss)
+    torch.cuda.synchronize()
+    ss = ss.cpu().numpy()
+    for i, ((dy, x), (M, N, T), (_, _, c)) in enumerate(zip(ops, shapes, dev)):
+        dw = c.cpu().numpy().view(np.uint16)
+        want = W.bf16_rne(W.wgrad_exact(dy, x))
+        assert np.array_equal(dw, want), f"problem {i}"
+        np.testing.assert_allclose(ss[off[i]:off[i + 1]], W.tile_sumsq(want), rtol=SS_RTOL,
+                                   atol=0, err_msg=f"problem {i}")
+        dw1, ss1 = run_wgrad(torch, dy, x)
+        assert np.array_equal(dw1, dw) and np.array_equal(ss1, ss[off[i]:off[i + 1]])
+
+
 def small_layer():
     return SW.WgradLayer("small-layer", ((512, 512), (512, 512), (512, 512), (512, 512),
                                          (1376, 512), (1376, 512), (512, 1376)), tokens=256)
