@@ -16,11 +16,18 @@
 // one feature.
 //
 // Tiling: one 256-lane workgroup per 256x256 output tile, four waves of
-// 128x128 (4x4 v_mfma_f32_32x32x16_bf16 blocks each), K steps of 64 with two
-// LDS stages: the global loads of step s+1 are in flight while the matrix
-// cores work on step s.  x is the matrix cores' A operand, so the four
-// accumulator rows a lane holds per group are four consecutive output
-// columns: each lane stores 8 contiguous bytes.
+// 128x128 (4x4 v_mfma_f32_32x32x16_bf16 blocks each), K steps of 64 split
+// into four slots of 16 (one matrix-core instruction per block and slot).
+// Two LDS buffers and one set of staging registers form the pipeline:
+// during step s the matrix cores work on buffer s%2, the staged operands of
+// step s+1 go to the other buffer while the global loads of step s+2 refill
+// the staging registers, so every global load has a whole step to land.
+// The fragments of slot k+1 are read from LDS while slot k's matrix-core
+// instructions run (two fragment register sets), and the workgroup meets at
+// one barrier per step, placed before the last slot's matrix-core work so
+// that the reads of the next buffer overlap it.  x is the matrix cores' A
+// operand, so the four accumulator rows a lane holds per group are four
+// consecutive output columns: each lane stores 8 contiguous bytes.
 #include "gnmr_internal.h"
 
 namespace gnmr {
@@ -41,6 +48,12 @@ constexpr int kStage = kWgBK * kLdsRow;      // elements per operand and stage
 constexpr int kChunks = kWgBK * kWgBN / 8 / kWgThreads;  // 16-byte chunks per lane, operand and stage
 static_assert(kWgBM == kWgBN, "square tiles: one load pattern serves both operands");
 static_assert(kChunks == 8, "load pattern");
+static_assert(kWgBK == 64, "four slots of 16 per K step");
+// sched_group_barrier instruction classes
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedVmemRead = 0x020;
+constexpr int kSchedDsRead = 0x100;
+constexpr int kSchedDsWrite = 0x200;
 
 // fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
 __device__ __forceinline__ uint32_t to_bf16(float v) {
@@ -91,34 +104,39 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
 
   // Global -> LDS: lane tid moves 16-byte chunk (row tid/32 + 8c, column
   // 8*(tid%32)) of each operand tile, c = 0..7, with buffer loads whose
-  // resource covers the rows of the current K step: rows past K and columns
-  // past M or N (whose offset is pushed past the resource) read as zero in
+  // resource covers the rows of one K step: rows past K and columns past M
+  // or N (whose offset is pushed past the resource) read as zero in
   // hardware, so every load is issued unconditionally (M, N multiples of 8:
-  // a chunk is all in or all out).
+  // a chunk is all in or all out).  Steps past the end get an empty
+  // resource: their loads read zeros without touching memory, and the
+  // buffers they fill are never read, which keeps the loop body free of
+  // branches.
   const int lrow = tid >> 5, lcol = (tid & 31) * 8;
   const uint32_t kOut = 0x80000000u;  // beyond any resource of this kernel
   const uint32_t xo = n0 + lcol < N ? uint32_t((lrow * N + n0 + lcol) * 2) : kOut;
   const uint32_t yo = m0 + lcol < M ? uint32_t((lrow * M + m0 + lcol) * 2) : kOut;
   u32x4 rx[kChunks], ry[kChunks];
-  auto gload = [&](int64_t k0) {
-    const int rows = K - k0 < kWgBK ? int(K - k0) : kWgBK;
-    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(x + k0 * N), 0, rows * N * 2, kBufferWord3);
-    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(dy + k0 * M), 0, rows * M * 2, kBufferWord3);
+  __amdgpu_buffer_rsrc_t xr, yr;
+  auto rsrc = [&](int64_t k0) {
+    const int64_t kb = k0 < K ? k0 : 0;
+    const int rws = k0 >= K ? 0 : (K - k0 < kWgBK ? int(K - k0) : kWgBK);
+    xr = __builtin_amdgcn_make_buffer_rsrc((void*)(x + kb * N), 0, rws * N * 2, kBufferWord3);
+    yr = __builtin_amdgcn_make_buffer_rsrc((void*)(dy + kb * M), 0, rws * M * 2, kBufferWord3);
+  };
+  auto gload = [&](int h) {  // chunks 4h .. 4h+3 of both operands
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
+    for (int c = 4 * h; c < 4 * h + 4; ++c) {
       rx[c] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xo + uint32_t(c * 16 * N), 0, 0));
       ry[c] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(yr, yo + uint32_t(c * 16 * M), 0, 0));
     }
   };
-  auto lstore = [&](int st) {
+  auto lstore = [&](int buf, int h) {
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      *(u32x4*)&lds[st][0][(lrow + 8 * c) * kLdsRow + lcol] = rx[c];
-      *(u32x4*)&lds[st][1][(lrow + 8 * c) * kLdsRow + lcol] = ry[c];
+    for (int c = 4 * h; c < 4 * h + 4; ++c) {
+      *(u32x4*)&lds[buf][0][(lrow + 8 * c) * kLdsRow + lcol] = rx[c];
+      *(u32x4*)&lds[buf][1][(lrow + 8 * c) * kLdsRow + lcol] = ry[c];
     }
   };
 
@@ -129,41 +147,95 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
   // the two reads h = 0, 1: the same k order for both operands.
   const int f_row = 8 * (lane >> 5) + ((lane & 15) >> 2);
   const int f_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  bf16x8 fx[2][4], fy[2][4];  // [register set][block]
+  auto rfrag = [&](int set, int buf, int kk) {
+    const uint16_t* lx = &lds[buf][0][f_row * kLdsRow + wn * 128 + f_col];
+    const uint16_t* ly = &lds[buf][1][f_row * kLdsRow + wm * 128 + f_col];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int o = kk * 16 * kLdsRow + 32 * b;
+      fx[set][b] = frag(lx + o, lx + o + 4 * kLdsRow);
+      fy[set][b] = frag(ly + o, ly + o + 4 * kLdsRow);
+    }
+  };
 
   f32x16 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
-
-  const int64_t nk = (K + kWgBK - 1) / kWgBK;  // 0 for an empty batch: dw = 0
-  if (nk > 0) {
-    gload(0);
-    lstore(0);
-  }
-  __syncthreads();
-  for (int64_t s = 0; s < nk; ++s) {
-    const int st = int(s & 1);
-    if (s + 1 < nk) gload((s + 1) * kWgBK);
-    const uint16_t* lx = &lds[st][0][f_row * kLdsRow + wn * 128 + f_col];
-    const uint16_t* ly = &lds[st][1][f_row * kLdsRow + wm * 128 + f_col];
+  auto mfma = [&](int set) {
 #pragma unroll
-    for (int kk = 0; kk < kWgBK / 16; ++kk) {
-      bf16x8 fx[4], fy[4];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int o = kk * 16 * kLdsRow + 32 * b;
-        fx[b] = frag(lx + o, lx + o + 4 * kLdsRow);
-        fy[b] = frag(ly + o, ly + o + 4 * kLdsRow);
-      }
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(fx[set][j], fy[set][i], acc[i][j], 0, 0, 0);
+  };
+  // Instruction order inside a slot (scheduling hints only): each
+  // matrix-core instruction is followed by two fragment reads for the next
+  // slot, then, in slots 0 and 1, by one LDS store and one global load.
+  auto order_reads = [] {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fx[j], fy[i], acc[i][j], 0, 0, 0);
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
     }
-    if (s + 1 < nk) lstore(st ^ 1);
+  };
+  auto order_stores = [] {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+    }
+  };
+
+  // 0 steps for an empty batch: dw = 0.  Prologue: step 0 in buffer 0,
+  // step 1 in the staging registers, the first slot's fragments read.
+  const int64_t nk = (K + kWgBK - 1) / kWgBK;
+  rsrc(0);
+  gload(0);
+  gload(1);
+  lstore(0, 0);
+  lstore(0, 1);
+  rsrc(kWgBK);
+  gload(0);
+  gload(1);
+  __syncthreads();
+  rfrag(0, 0, 0);
+  for (int64_t s = 0; s < nk; ++s) {
+    const int buf = int(s & 1);
+    // slot 0: stage half of step s+1, load half of step s+2
+    rfrag(1, buf, 1);
+    lstore(buf ^ 1, 0);
+    rsrc((s + 2) * kWgBK);
+    gload(0);
+    mfma(0);
+    order_reads();
+    order_stores();
+    // slot 1: the other halves
+    rfrag(0, buf, 2);
+    lstore(buf ^ 1, 1);
+    gload(1);
+    mfma(1);
+    order_reads();
+    order_stores();
+    // slot 2
+    rfrag(1, buf, 3);
+    mfma(0);
+    order_reads();
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 8, 0);
+    // slot 3: every wave has stored its part of step s+1 and read its last
+    // fragments of buffer s%2 (the barrier waits for both), so buffer
+    // (s+1)%2 is complete and buffer s%2 free for step s+2
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    rfrag(0, buf ^ 1, 0);
+    mfma(1);
+    order_reads();
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 8, 0);
   }
 
   // Epilogue: accumulator register r of block (i, j) holds output row
