@@ -145,13 +145,13 @@ def library_reduce_probe(torch, buf, lay, w, reps: int = 5):
             "GBs": round(w.bytes_per_step / (ms * 1e-3) / 1e9, 1)}
 
 
-def measured_traffic(workload: str):
-    """K1's HBM bytes per launch from the committed rocprofv3 counter summary,
-    or None when it is for another workload or the kernel source has changed
-    since the counters were taken."""
+def measured_traffic(profile: str, sources, workload: str):
+    """A kernel's HBM bytes per launch from its committed rocprofv3 counter
+    summary (profiles/<profile>), or None when the summary is for another
+    workload or the kernel source has changed since the counters were taken."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", f"k1_sumsq_{workload}_bf16_traffic.md")
+    path = os.path.join(ROOT, "profiles", profile)
     if not os.path.exists(path):
         return None
     kv = {}
@@ -160,7 +160,7 @@ def measured_traffic(workload: str):
             k, _, v = line.strip().partition("=")
             kv[k] = v
     src = b"".join(open(os.path.join(ROOT, "paper_2606_00539_amd", "csrc", f), "rb").read()
-                   for f in K1_SOURCES)
+                   for f in sources)
     if kv.get("kernel_source_sha256_16") != hashlib.sha256(src).hexdigest()[:16]:
         return None
     if kv.get("workload") != workload:
@@ -337,7 +337,11 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
                                f"{tokens} tokens, bf16", "units": U, "tokens": tokens,
                    "flops_per_step": L.flops, "grad_bytes": L.grad_bytes},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0,
-                     "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(tflops / 2500.0, 4),
+                     "traffic": measured_traffic("k5_wgrad_llama2-13b_layer.md", ("k5_wgrad.hip",),
+                                                 L.name),
+                     "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "algorithmic_bytes": L.operand_bytes + L.grad_bytes,
                      "kernel": "k5_wgrad", "kernel_ms_per_step": round(ms_k5, 4)},
         "unfused": {"ms_per_step": round(ms_unfused, 4),
                     "hipblaslt_gemms_ms": round(ms_blas, 4),
@@ -455,7 +459,7 @@ def main():
     gbs = w.bytes_per_step / (elapsed / args.steps) / 1e9
     k1_ms = prof["ms_sumsq"] / max(prof["steps"], 1)
     k1_gbs = w.bytes_per_step / (k1_ms * 1e-3) / 1e9
-    traffic = measured_traffic(w.name)
+    traffic = measured_traffic(f"k1_sumsq_{w.name}_bf16_traffic.md", K1_SOURCES, w.name)
     roofline = {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",

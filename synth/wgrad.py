@@ -67,6 +67,11 @@ class WgradLayer:
     def grad_bytes(self) -> int:
         return sum(2 * o * i for o, i in self.shapes)
 
+    @property
+    def operand_bytes(self) -> int:
+        """dy and x of every GEMM, bf16, each read once."""
+        return sum(2 * self.tokens * (o + i) for o, i in self.shapes)
+
     def dy_scale(self, t: int, b: int) -> float:
         """Per-unit output-gradient scale: LogUniform[1e-4, 1e-2] per unit
         (drawn once from the seed), x10 in unit (t mod 7) at every step t
