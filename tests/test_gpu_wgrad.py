@@ -249,3 +249,66 @@ def test_partials_binding_errors():
         ctl.step_from_partials(parts, 1.5, 1.5)
         out = ctl.query()
         np.testing.assert_allclose(out["norm"], [2.0, 2.0, 3.0], rtol=1e-15)
+
+
+def test_layer_fullsize_batched_step_matches_oracle():
+    """The benchmark's launch configuration: the seven weight-gradient GEMMs
+    of a LLaMA-2-13B layer at 4,096 tokens in one batched launch, then the
+    controller step from the tile partials, for two steps.  Sampled dw
+    elements are computed one by one by the oracle; sampled tiles and every
+    unit norm are checked against float64 sums over the stored gradient; the
+    step's decisions against the oracle controller."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller, gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    L = SW.llama2_13b_layer(4096)
+    U, T = L.num_units, L.tokens
+    numel = [o * i for o, i in L.shapes]
+    off = np.concatenate([[0], np.cumsum(numel)]).astype(np.int64)
+    grads = torch.empty(int(off[-1]), dtype=torch.int16, device="cuda")
+    dws = [grads[int(off[b]):int(off[b + 1])].view(o, i) for b, (o, i) in enumerate(L.shapes)]
+    tiles = [gnmr_wgrad_num_tiles(o, i) for o, i in L.shapes]
+    poff = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    parts = torch.full((int(poff[-1]),), float("nan"), dtype=torch.float32, device="cuda")
+    ptrs = [d.data_ptr() for d in dws]
+    ora = Oracle(U, window=5, max_o=2, lock_len=4, eps=1e-12)
+    rng = np.random.default_rng(13)
+    with Controller(U, 5, 2, 4, 1e-12, np.arange(U + 1), numel, [1] * U, ptrs) as ctl:
+        ctl.bind_partials(poff)
+        for t in (1, 2):
+            say(f"wgrad 13B layer batched, step {t}")
+            ops = [SW.operands(L.seed, t, b, T, o, i, dy_scale=L.dy_scale(t, b))
+                   for b, (o, i) in enumerate(L.shapes)]
+            dev = [(to_dev(torch, dy), to_dev(torch, x)) for dy, x in ops]
+            gnmr_wgrad_sumsq_batched([(a, c, dws[b], T, o, i) for b, ((a, c), (o, i))
+                                      in enumerate(zip(dev, L.shapes))], parts)
+            alpha, beta = (1.5 if t == 1 else 1.1), 1.5
+            ctl.step_from_partials(parts, alpha, beta)
+            out = ctl.query()
+            ss = parts.cpu().numpy()
+            norms = np.zeros(U)
+            for b, ((dy, x), (o, i)) in enumerate(zip(ops, L.shapes)):
+                dw = dws[b].cpu().numpy().view(np.uint16)
+                rows = rng.choice(o, 16, replace=False)
+                cols = rng.choice(i, 16, replace=False)
+                exact = W.wgrad_exact(dy[:, rows], x[:, cols])
+                bound = W.error_bound(dy[:, rows], x[:, cols], exact)
+                err = np.abs(W.widen_bf16(dw[np.ix_(rows, cols)]) - exact)
+                assert np.all(err <= bound), f"t={t} unit {b}: dw outside the bound"
+                ts = ss[poff[b]:poff[b + 1]]
+                tn = -(-i // 256)
+                for tile in rng.choice(ts.size, 3, replace=False):
+                    a, c = divmod(int(tile), tn)
+                    blk = dw[a * 256:(a + 1) * 256, c * 256:(c + 1) * 256]
+                    np.testing.assert_allclose(ts[tile], W.tile_sumsq(blk)[0], rtol=SS_RTOL,
+                                               atol=0, err_msg=f"t={t} unit {b} tile {tile}")
+                norms[b] = W.unit_norm(dw)
+                del dw
+            ref = ora.step(norms, alpha, beta)
+            g, d = ref.gnmr / alpha, ref.dgnmr / beta
+            assert np.all(np.abs(g - 1) > 1e-3) and np.all(np.abs(d - 1) > 1e-3), f"t={t}"
+            # fp32 tile sums (each within 264 roundings) against the float64
+            # norm of the same stored values: relative 264 * 2^-24 / 2 on n,
+            # at most twice that on a ratio of two norms
+            assert_step_matches(out, ref, rtol=2 * SS_RTOL, what=f"13B layer t={t}")
+            assert out["stats"]["t"] == t
