@@ -160,8 +160,8 @@ gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
  *   dw[o][i] = bf16_rne( sum_t dy[t][o] * x[t][i] )     (fp32 accumulation)
  * dy: device [tokens][out_features] bf16, x: device [tokens][in_features]
  * bf16, dw: device [out_features][in_features] bf16, all row-major and
- * 16-byte aligned; out_features and in_features multiples of 8; tokens >= 0
- * (0 gives dw = 0).  tile_sumsq: device float [gnmr_wgrad_num_tiles(out,
+ * 16-byte aligned; out_features and in_features multiples of 8 below 2^24;
+ * tokens >= 0 (0 gives dw = 0).  tile_sumsq: device float [gnmr_wgrad_num_tiles(out,
  * in)], written with the fp32 sum of float(dw)^2 over each 256x256 output
  * tile (row-major tile order, ragged edge tiles included), each in a fixed
  * order: deterministic.  The caller owns every buffer; dw must not overlap

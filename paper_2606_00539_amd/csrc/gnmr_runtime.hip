@@ -538,8 +538,9 @@ gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t
       return fail(GNMR_E_INVALID, "out_features and in_features must be > 0, tokens >= 0");
     if (q.out_features % 8 != 0 || q.in_features % 8 != 0)
       return fail(GNMR_E_INVALID, "out_features and in_features must be multiples of 8");
-    if (q.out_features > (1 << 24) || q.in_features > (1 << 24))
-      return fail(GNMR_E_INVALID, "out_features and in_features must be <= 2^24");
+    // K5 addresses one K step of an operand (64 rows) with 32-bit byte offsets
+    if (q.out_features >= (1 << 24) || q.in_features >= (1 << 24))
+      return fail(GNMR_E_INVALID, "out_features and in_features must be < 2^24");
     if (q.dw == nullptr || (q.tokens > 0 && (q.dy == nullptr || q.x == nullptr)))
       return fail(GNMR_E_INVALID, "dy, x and dw must be device pointers");
     if ((reinterpret_cast<uintptr_t>(q.dy) | reinterpret_cast<uintptr_t>(q.x) |

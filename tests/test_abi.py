@@ -105,6 +105,7 @@ def test_bench_refuses_more_than_one_gpu():
 @pytest.mark.parametrize("bad", [
     dict(out_f=12), dict(in_f=4), dict(out_f=0), dict(in_f=-8), dict(tokens=-1),
     dict(dy=0), dict(x=0), dict(dw=0), dict(ss=0), dict(dy=4096 + 8), dict(dw=8192 + 2),
+    dict(in_f=1 << 24), dict(out_f=1 << 24),
 ])
 def test_wgrad_rejects_bad_arguments(bad):
     # every case fails in the argument checks, before any device call
