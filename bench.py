@@ -145,6 +145,32 @@ def library_reduce_probe(torch, buf, lay, w, reps: int = 5):
             "GBs": round(w.bytes_per_step / (ms * 1e-3) / 1e9, 1)}
 
 
+def read_ceiling_probe(torch, buf, w, stream, reps: int = 5):
+    """Plain read-reduce kernels over the same gradient bytes (grid-stride,
+    and one 64 KiB block per workgroup in XCD-contiguous order): the read
+    rate a minimal kernel reaches on this buffer in this run."""
+    from synth.gpu import ReadProbe
+
+    rp = ReadProbe()
+    out = {}
+    s = stream.cuda_stream
+    for v, name in rp.VARIANTS.items():
+        parts = torch.empty(rp.num_partials(w.bytes_per_step, v), dtype=torch.float32,
+                            device="cuda")
+        for _ in range(2):
+            rp.run(buf.data_ptr(), w.bytes_per_step, parts.data_ptr(), v, s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            rp.run(buf.data_ptr(), w.bytes_per_step, parts.data_ptr(), v, s)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[name] = {"ms": round(ms, 4), "GBs": round(w.bytes_per_step / (ms * 1e-3) / 1e9, 1)}
+    return out
+
+
 def measured_traffic(profile: str, sources, workload: str):
     """A kernel's HBM bytes per launch from its committed rocprofv3 counter
     summary (profiles/<profile>), or None when the summary is for another
@@ -483,6 +509,10 @@ def main():
         "roofline": roofline,
         "step_us_spread": spread,
     }
+    if w.bytes_per_step % 16 == 0:
+        result["read_ceiling_probe"] = read_ceiling_probe(torch, buf, w, stream)
+        best = max(v["GBs"] for v in result["read_ceiling_probe"].values())
+        result["roofline"]["frac_of_read_probe"] = round(k1_gbs / best, 4)
     probe = library_reduce_probe(torch, buf, lay, w)
     if probe is not None:
         result["library_reduce_probe"] = probe

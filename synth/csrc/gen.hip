@@ -95,3 +95,107 @@ int synth_fill(const synth_job* jobs, int64_t njobs, const float* d_table, void*
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Read-ceiling probes (benchmark reference points, not part of the method):
+// plain read-reduce kernels over a contiguous 16-byte-aligned buffer, each
+// lane summing the fp32 squares of the words it reads, one fp32 partial per
+// workgroup.  They show the read rate a minimal kernel reaches on the same
+// bytes as the gradient pass.
+// ---------------------------------------------------------------------------
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 g_vec;
+constexpr int kProbeUnroll = 16;
+constexpr int64_t kProbeBlockVecs = int64_t(kBlock) * kProbeUnroll;   // 64 KiB per workgroup
+
+__device__ __forceinline__ float sq4(const u32x4& v) {
+  float a = __uint_as_float(v.x), b = __uint_as_float(v.y), c = __uint_as_float(v.z),
+        d = __uint_as_float(v.w);
+  return (a * a + b * b) + (c * c + d * d);
+}
+
+__device__ __forceinline__ void block_partial(float s, float* out) {
+  __shared__ float red[kBlock / 64];
+  for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) out[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+// Variant 0: grid-stride loop, 16-byte non-temporal loads, 8 in flight per lane.
+__global__ __launch_bounds__(kBlock) void probe_grid_stride(const g_vec* __restrict__ p,
+                                                            int64_t nvec, float* out) {
+  const int64_t stride = int64_t(gridDim.x) * kBlock;
+  float s = 0.f;
+  int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  for (; i + 7 * stride < nvec; i += 8 * stride) {
+    u32x4 v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = __builtin_nontemporal_load(p + i + k * stride);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += sq4(v[k]);
+  }
+  for (; i < nvec; i += stride) s += sq4(__builtin_nontemporal_load(p + i));
+  block_partial(s, out);
+}
+
+// Variant 1: one 64 KiB block per workgroup, all 16 loads of a lane issued
+// before the first is used, blocks dealt to the eight XCDs in contiguous
+// runs (workgroup w runs on XCD w % 8) -- the gradient pass's read pattern
+// without its work-item table.
+__global__ __launch_bounds__(kBlock) void probe_blocked(const g_vec* __restrict__ p, int64_t nvec,
+                                                        float* out) {
+  const uint32_t nblk = gridDim.x, w = blockIdx.x;
+  const uint32_t x = w % 8, j = w / 8, q = nblk / 8, r = nblk % 8;
+  const int64_t blk = int64_t(x) * q + (x < r ? x : r) + j;
+  const int64_t v0 = blk * kProbeBlockVecs;
+  const int64_t n = nvec - v0 < kProbeBlockVecs ? nvec - v0 : kProbeBlockVecs;
+  u32x4 v[kProbeUnroll];
+#pragma unroll
+  for (int k = 0; k < kProbeUnroll; ++k) {
+    const int64_t i = threadIdx.x + int64_t(k) * kBlock;
+    v[k] = __builtin_nontemporal_load(p + v0 + (i < n ? i : n - 1));
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < kProbeUnroll; ++k)
+    if (threadIdx.x + int64_t(k) * kBlock < n) s += sq4(v[k]);
+  block_partial(s, out);
+}
+
+}  // namespace
+
+extern "C" {
+
+// Number of fp32 partials synth_read_probe writes for `bytes` and `variant`.
+int64_t synth_read_probe_partials(int64_t bytes, int32_t variant) {
+  const int64_t nvec = bytes / 16;
+  if (nvec <= 0) return 0;
+  return variant == 0 ? int64_t(256) * 8 : (nvec + kProbeBlockVecs - 1) / kProbeBlockVecs;
+}
+
+// Launches one read-reduce pass over `bytes` (a multiple of 16) at the
+// 16-byte-aligned device address `p` on `stream`; `partials` holds
+// synth_read_probe_partials(bytes, variant) floats.  Returns 0 or a hipError_t
+// (1 = hipErrorInvalidValue for bad arguments).
+int synth_read_probe(const void* p, int64_t bytes, float* partials, int32_t variant,
+                     void* stream) {
+  if (p == nullptr || partials == nullptr || bytes <= 0 || bytes % 16 != 0 ||
+      reinterpret_cast<uintptr_t>(p) % 16 != 0 || (variant != 0 && variant != 1))
+    return int(hipErrorInvalidValue);
+  const int64_t nvec = bytes / 16;
+  const int64_t grid = synth_read_probe_partials(bytes, variant);
+  if (grid > int64_t(UINT32_MAX)) return int(hipErrorInvalidValue);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (variant == 0)
+    hipLaunchKernelGGL(probe_grid_stride, dim3(unsigned(grid)), dim3(kBlock), 0, st,
+                       (const g_vec*)reinterpret_cast<uintptr_t>(p), nvec, partials);
+  else
+    hipLaunchKernelGGL(probe_blocked, dim3(unsigned(grid)), dim3(kBlock), 0, st,
+                       (const g_vec*)reinterpret_cast<uintptr_t>(p), nvec, partials);
+  return int(hipGetLastError());
+}
+
+}  // extern "C"

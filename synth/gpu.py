@@ -53,3 +53,29 @@ class Generator:
         rc = self.lib.synth_fill(arr, len(jobs), self.table.data_ptr(), stream)
         if rc != 0:
             raise RuntimeError(f"synth_fill failed with hipError {rc}")
+
+
+class ReadProbe:
+    """Plain read-reduce kernels over a contiguous device buffer (the
+    benchmark's read-ceiling reference points): variant 0 is a grid-stride
+    loop, variant 1 one 64 KiB block per workgroup in XCD-contiguous order."""
+
+    VARIANTS = {0: "grid_stride_nt", 1: "blocked_nt_xcd"}
+
+    def __init__(self):
+        if not os.path.exists(_LIB):
+            raise RuntimeError(f"{_LIB} is not built (run __graft_entry__.build())")
+        self.lib = ctypes.CDLL(_LIB)
+        self.lib.synth_read_probe_partials.restype = ctypes.c_int64
+        self.lib.synth_read_probe_partials.argtypes = [ctypes.c_int64, ctypes.c_int32]
+        self.lib.synth_read_probe.restype = ctypes.c_int
+        self.lib.synth_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                              ctypes.c_int32, ctypes.c_void_p]
+
+    def num_partials(self, nbytes: int, variant: int) -> int:
+        return int(self.lib.synth_read_probe_partials(int(nbytes), int(variant)))
+
+    def run(self, ptr: int, nbytes: int, partials_ptr: int, variant: int, stream: int = 0):
+        rc = self.lib.synth_read_probe(ptr, int(nbytes), partials_ptr, int(variant), stream)
+        if rc != 0:
+            raise RuntimeError(f"synth_read_probe failed with hipError {rc}")
