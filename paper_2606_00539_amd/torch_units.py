@@ -86,3 +86,152 @@ class TorchUnits:
 
     def close(self):
         self.ctl.close()
+
+
+_FUNCTION = None
+
+
+def _fused_linear_function():
+    """The autograd function of a linear layer whose weight gradient comes
+    from gnmr_wgrad_sumsq (built on first use, so that importing this module
+    does not import torch)."""
+    global _FUNCTION
+    if _FUNCTION is None:
+        import torch
+
+        class FusedWgradLinear(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, x, weight, units, index):
+                ctx.save_for_backward(x, weight)
+                ctx.units, ctx.index = units, index
+                return torch.matmul(x, weight.t())
+
+            @staticmethod
+            def backward(ctx, dy):
+                x, weight = ctx.saved_tensors
+                dx = torch.matmul(dy, weight) if ctx.needs_input_grad[0] else None
+                dw = ctx.units._weight_grad(ctx.index, dy, x) if ctx.needs_input_grad[1] else None
+                return dx, dw, None, None
+
+        _FUNCTION = FusedWgradLinear
+    return _FUNCTION
+
+
+def _kernel_operand(t, features: int):
+    """t as a contiguous, 16-byte-aligned [tokens][features] bf16 matrix
+    (a copy only when the view is neither)."""
+    t = t.reshape(-1, features)
+    if not t.is_contiguous():
+        t = t.contiguous()
+    if t.data_ptr() % 16:
+        t = t.clone()
+    return t
+
+
+class FusedWgradUnits:
+    """Bias-free or biased bf16 `torch.nn.Linear` layers as GNMR units whose
+    norms come from the weight-gradient GEMM itself (K5, the sum of squares
+    in its epilogue): each layer's forward is routed through an autograd
+    function whose backward computes dW = dy^T x with gnmr_wgrad_sumsq into a
+    fresh tensor that becomes `weight.grad`, and writes the layer's tile
+    partials; `step()` then runs the controller from those partials
+    (gnmr_step_from_partials), so the gradients are never re-read for their
+    norms.  Only the weight is the unit; a bias gradient is computed by torch.
+
+    Each layer must run forward exactly once per step, and `weight.grad` must
+    be None before backward (zero_grad(set_to_none=True)): if autograd
+    accumulated into an existing gradient, the partials would describe only
+    the last product, and `step()` raises instead.
+    """
+
+    def __init__(self, named_linears, window: int = 5, max_o: int = 8, lock_len: int = 8,
+                 eps: float = 1e-12, recoverable=None, budget_mode: int = GNMR_BUDGET_ACTIVE,
+                 warmup_steps: int = 0, stream=None):
+        import torch
+
+        from .binding import gnmr_wgrad_num_tiles
+
+        self.unit_names, self.modules, self.shapes = [], [], []
+        for name, m in named_linears:
+            w = m.weight
+            if w.dtype != torch.bfloat16 or not w.is_cuda:
+                raise TypeError(f"{name}: the weight must be a bf16 tensor on a HIP device")
+            o, i = w.shape
+            if o % 8 or i % 8 or o >= 1 << 24 or i >= 1 << 24:
+                raise ValueError(f"{name}: features must be multiples of 8 below 2^24, got {o}x{i}")
+            self.unit_names.append(name)
+            self.modules.append(m)
+            self.shapes.append((o, i))
+        if not self.modules:
+            raise ValueError("no linear layer given")
+        U = len(self.modules)
+        tiles = [gnmr_wgrad_num_tiles(o, i) for o, i in self.shapes]
+        self.part_off = np.zeros(U + 1, dtype=np.int64)
+        self.part_off[1:] = np.cumsum(tiles)
+        self.partials = torch.zeros(int(self.part_off[-1]), dtype=torch.float32,
+                                    device=self.modules[0].weight.device)
+        rec = None
+        if recoverable is not None:
+            rec = np.array([1 if recoverable(u) else 0 for u in self.unit_names], np.uint8)
+        self.ctl = Controller(U, window, max_o, lock_len, eps, np.zeros(U + 1, np.int64), [], [],
+                              None, rec, stream, budget_mode, warmup_steps)
+        self.ctl.bind_partials(self.part_off)
+        self._produced = [None] * U   # data pointer of each layer's dW this step
+        self._saved_forward = []
+        for b, m in enumerate(self.modules):
+            self._saved_forward.append(m.__dict__.get("forward"))
+            m.forward = self._routed_forward(m, b)
+
+    def _routed_forward(self, m, b):
+        fn = _fused_linear_function()
+
+        def forward(x):
+            y = fn.apply(x, m.weight, self, b)
+            return y if m.bias is None else y + m.bias
+        return forward
+
+    def _weight_grad(self, b, dy, x):
+        import torch
+
+        from .binding import gnmr_wgrad_sumsq
+
+        o, i = self.shapes[b]
+        if dy.dtype != torch.bfloat16 or x.dtype != torch.bfloat16:
+            raise TypeError(f"{self.unit_names[b]}: activations and gradients must be bf16")
+        dy2, x2 = _kernel_operand(dy, o), _kernel_operand(x, i)
+        dw = torch.empty((o, i), dtype=torch.bfloat16, device=dy.device)
+        lo, hi = int(self.part_off[b]), int(self.part_off[b + 1])
+        gnmr_wgrad_sumsq(dy2, x2, dw, dy2.shape[0], o, i, self.partials[lo:hi],
+                         torch.cuda.current_stream())
+        self._produced[b] = dw.data_ptr()
+        return dw
+
+    def step(self, alpha_t: float, beta_t: float, stream=None) -> None:
+        """One controller step from this backward's tile partials (asynchronous)."""
+        for b, m in enumerate(self.modules):
+            g = m.weight.grad
+            if self._produced[b] is None or g is None or g.data_ptr() != self._produced[b]:
+                raise RuntimeError(
+                    f"{self.unit_names[b]}: weight.grad is not the gradient the fused backward "
+                    "produced this step (layer unused, or accumulated into an existing grad; "
+                    "call zero_grad(set_to_none=True) before backward)")
+        self.ctl.step_from_partials(self.partials, alpha_t, beta_t, stream)
+        self._produced = [None] * len(self.modules)
+
+    def query(self, stream=None) -> dict:
+        out = self.ctl.query(stream)
+        out["units"] = self.unit_names
+        return out
+
+    def recovery_set(self, stream=None) -> list:
+        m = self.ctl.query(stream)["mask"]
+        return [u for u, a in zip(self.unit_names, m) if a]
+
+    def close(self):
+        for m, f in zip(self.modules, self._saved_forward):
+            if f is None:
+                m.__dict__.pop("forward", None)
+            else:
+                m.forward = f
+        self._saved_forward = [None] * len(self.modules)
+        self.ctl.close()

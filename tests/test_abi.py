@@ -139,3 +139,15 @@ def test_wgrad_batched_rejects_a_bad_problem_before_launching():
     assert e.value.status == B.GNMR_E_INVALID
     with pytest.raises(GnmrError):
         B.gnmr_wgrad_sumsq_batched([good], 0)
+
+
+def test_fused_wgrad_units_rejects_unsupported_layers():
+    # argument checks before any device work: fp32 or host weights, odd shapes
+    import torch
+
+    from paper_2606_00539_amd.torch_units import FusedWgradUnits
+
+    with pytest.raises(TypeError):
+        FusedWgradUnits([("a", torch.nn.Linear(16, 16, bias=False))])
+    with pytest.raises(ValueError):
+        FusedWgradUnits([])

@@ -312,3 +312,83 @@ def test_layer_fullsize_batched_step_matches_oracle():
             # at most twice that on a ratio of two norms
             assert_step_matches(out, ref, rtol=2 * SS_RTOL, what=f"13B layer t={t}")
             assert out["stats"]["t"] == t
+
+
+def _tiny_block(torch, seed):
+    """Seven bias-free bf16 projections shaped like a small decoder layer,
+    each used once per forward."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    names = ("q", "k", "v", "o", "gate", "up", "down")
+    shapes = ((256, 256), (256, 256), (256, 256), (256, 256), (688, 256), (688, 256),
+              (256, 688))
+    mods = torch.nn.ModuleDict()
+    for n, (o, i) in zip(names, shapes):
+        lin = torch.nn.Linear(i, o, bias=False)
+        with torch.no_grad():
+            lin.weight.copy_(torch.randn(o, i, generator=g) * (1.0 / i ** 0.5))
+        mods[n] = lin
+    return mods.to(device="cuda", dtype=torch.bfloat16)
+
+
+def _block_forward(m, x, q_gain=1.0):
+    a = m["q"](x * q_gain) + m["k"](x) + m["v"](x)
+    h = m["o"](a)
+    return m["down"](m["gate"](h) * m["up"](h))
+
+
+def test_fused_wgrad_units_in_autograd_match_torch_and_k1():
+    """FusedWgradUnits routes a model's linear layers through K5 in backward:
+    the weight gradients agree with torch's own backward within two bf16
+    roundings, and the controller step from the tile partials makes the same
+    decisions as the K1 step (TorchUnits) over the same stored gradients."""
+    import copy
+
+    torch = require_gpu()
+    from paper_2606_00539_amd.torch_units import FusedWgradUnits, TorchUnits
+
+    fused_m = _tiny_block(torch, 7)
+    ref_m = copy.deepcopy(fused_m)
+    fused = FusedWgradUnits(list(fused_m.items()), max_o=2, lock_len=2)
+    k1 = TorchUnits(list(fused_m.named_parameters()), max_o=2, lock_len=2)
+    ora = Oracle(7, window=5, max_o=2, lock_len=2, eps=1e-12)
+    g = torch.Generator(device="cpu").manual_seed(3)
+    try:
+        for t in range(1, 9):
+            say(f"fused autograd step {t}")
+            x = (torch.randn(200, 256, generator=g)).to("cuda", torch.bfloat16)
+            for model in (fused_m, ref_m):
+                model.zero_grad(set_to_none=True)
+                # a x5 spike in the q projection's gradient at step 6
+                y = _block_forward(model, x, q_gain=5.0 if t == 6 else 1.0)
+                loss = y.float().square().mean()
+                loss.backward()
+            # torch's own backward of the same model: dW within two bf16 roundings
+            for n in fused_m:
+                a = fused_m[n].weight.grad.float()
+                b = ref_m[n].weight.grad.float()
+                tol = 2.0 ** -7 * b.abs() + 1e-3 * b.abs().max()
+                assert bool(((a - b).abs() <= tol).all()), f"t={t} {n}: dW differs from torch"
+            alpha, beta = (1.5 if t == 1 else 1.1), 1.5
+            fused.step(alpha, beta)
+            k1.step(alpha, beta)
+            out_f, out_k = fused.query(), k1.query()
+            norms = np.array([W.unit_norm(fused_m[n].weight.grad.view(torch.int16).cpu().numpy()
+                                          .view(np.uint16)) for n in fused_m])
+            ref = ora.step(norms, alpha, beta)
+            gm, dm = ref.gnmr / alpha, ref.dgnmr / beta
+            assert np.all(np.abs(gm - 1) > 1e-4) and np.all(np.abs(dm - 1) > 1e-4), f"t={t}"
+            r = np.sort(ref.risk[ref.risk > 1.0])[::-1]
+            if r.size > 2:      # the cap binds: the 2nd and 3rd risks are clearly apart
+                assert (r[1] - r[2]) / r[1] > 1e-4, f"t={t}: near-tie at the cut"
+            assert_step_matches(out_f, ref, rtol=2 * SS_RTOL, what=f"fused t={t}")
+            assert_step_matches(out_k, ref, rtol=1e-5, what=f"k1 t={t}")
+            if t == 6:
+                assert out_f["mask"][0] == 1, "the q spike must send q to the recovery path"
+        # accumulating into an existing gradient is refused, not silently wrong
+        y = _block_forward(fused_m, x)
+        y.float().square().mean().backward()
+        with pytest.raises(RuntimeError, match="zero_grad"):
+            fused.step(1.1, 1.5)
+    finally:
+        fused.close()
+        k1.close()
