@@ -392,3 +392,71 @@ def test_fused_wgrad_units_in_autograd_match_torch_and_k1():
     finally:
         fused.close()
         k1.close()
+
+
+def test_fused_layer_step_captured_in_a_graph_replays_like_eager():
+    """The batched K5 launch and the step from its partials, captured once in
+    a HIP graph and replayed: with fresh operands copied in between replays
+    (eager work and synchronisations in between), every replay's gradients,
+    masks, locks and ratios are bit-identical to the same step run eagerly."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller, gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    L = small_layer()
+    U, T = L.num_units, L.tokens
+    steps, capture_at = 10, 3
+    numel = [o * i for o, i in L.shapes]
+    tiles = [gnmr_wgrad_num_tiles(o, i) for o, i in L.shapes]
+    poff = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    dys = [torch.empty((T, o), dtype=torch.int16, device="cuda") for o, _ in L.shapes]
+    xs = [torch.empty((T, i), dtype=torch.int16, device="cuda") for _, i in L.shapes]
+
+    def side_buffers():
+        dws = [torch.empty((o, i), dtype=torch.int16, device="cuda") for o, i in L.shapes]
+        parts = torch.empty(int(poff[-1]), dtype=torch.float32, device="cuda")
+        return dws, parts
+
+    def problems(dws):
+        return [(dys[b], xs[b], dws[b], T, o, i) for b, (o, i) in enumerate(L.shapes)]
+
+    def load(t):
+        for b, (o, i) in enumerate(L.shapes):
+            dy, x = SW.operands(L.seed, t, b, T, o, i, dy_scale=L.dy_scale(t, b))
+            dys[b].copy_(torch.from_numpy(dy.view(np.int16)))
+            xs[b].copy_(torch.from_numpy(x.view(np.int16)))
+        torch.cuda.synchronize()
+
+    (dws_e, parts_e), (dws_g, parts_g) = side_buffers(), side_buffers()
+    mk = lambda: Controller(U, 5, 2, 3, 1e-12, np.zeros(U + 1, np.int64), [], [])
+    with mk() as eager, mk() as graphed:
+        eager.bind_partials(poff)
+        graphed.bind_partials(poff)
+        graph, side = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+        for t in range(1, steps + 1):
+            say(f"fused graph t={t}")
+            load(t)
+            alpha = 1.5 if t == 1 else 1.1
+            gnmr_wgrad_sumsq_batched(problems(dws_e), parts_e)
+            eager.step_from_partials(parts_e, alpha, 1.5)
+            if t < capture_at:
+                gnmr_wgrad_sumsq_batched(problems(dws_g), parts_g)
+                graphed.step_from_partials(parts_g, alpha, 1.5)
+            else:
+                if t == capture_at:
+                    torch.cuda.synchronize()
+                    with torch.cuda.stream(side):
+                        with torch.cuda.graph(graph, stream=side):
+                            gnmr_wgrad_sumsq_batched(problems(dws_g), parts_g, side)
+                            graphed.step_from_partials(parts_g, 1.1, 1.5, side)
+                    torch.cuda.synchronize()
+                    assert graphed.query()["stats"]["t"] == capture_at - 1
+                graph.replay()
+            torch.cuda.synchronize()
+            oe, og = eager.query(), graphed.query()
+            for b in range(U):
+                assert torch.equal(dws_e[b], dws_g[b]), f"t={t} unit {b}: dw"
+            assert torch.equal(parts_e, parts_g), f"t={t}: tile partials"
+            for k in ("mask", "lock", "norm", "gnmr", "dgnmr", "risk"):
+                assert np.array_equal(oe[k], og[k]), f"t={t}: {k}"
+            assert oe["stats"] == og["stats"], f"t={t}: stats"
+        assert og["stats"]["t"] == steps
