@@ -176,9 +176,13 @@ gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t to
  * layer) in one launch, so that their tiles share the machine: each problem
  * as in gnmr_wgrad_sumsq; problem i's tile sums start at tile_sumsq + the
  * tile counts of problems 0..i-1 (the layout gnmr_bind_partials expects with
- * one unit per problem).  `problems` is a host array, read before return;
- * every check of gnmr_wgrad_sumsq applies to each problem, and nothing is
- * launched if one fails. */
+ * one unit per problem).  A problem with accumulate = 1 adds its product to
+ * the gradient already stored in dw (gradient accumulation over
+ * micro-batches): dw = bf16_rne(fp32(dw + product)), one fp32 addition and
+ * one rounding to bf16, and its tile sums are those of the accumulated dw.
+ * `problems` is a host array, read before return; every check of
+ * gnmr_wgrad_sumsq applies to each problem (and accumulate is 0 or 1), and
+ * nothing is launched if one fails. */
 typedef struct {
   const void* dy;        /* device [tokens][out_features] bf16 */
   const void* x;         /* device [tokens][in_features] bf16  */
@@ -186,6 +190,8 @@ typedef struct {
   int64_t tokens;
   int32_t out_features;
   int32_t in_features;
+  int32_t accumulate;    /* 0: dw = product; 1: dw += product */
+  int32_t reserved;      /* 0 */
 } gnmr_wgrad_problem;
 gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems,
                                      int32_t num_problems, float* tile_sumsq,

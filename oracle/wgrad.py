@@ -24,7 +24,10 @@ Readings (also in DESIGN.md):
     result obeys: |q - exact| <= 2^-8 (|exact| + g S) + g S, S = |dy|^T |x|,
     g = K u / (1 - K u) with u = 2^-23 (one unit of fp32 precision per
     addition, which also covers directed rounding inside the accumulator),
-    plus 2^-133 for bf16 underflow.
+    plus 2^-133 for bf16 underflow;
+  * gradient accumulation over micro-batches: the kernel adds its fp32
+    accumulation to the stored bf16 gradient in fp32 (one rounding) and
+    rounds the sum to bf16 once; error_bound_accumulate() states the bound.
 """
 from __future__ import annotations
 
@@ -95,6 +98,31 @@ def error_bound(dy_bits: np.ndarray, x_bits: np.ndarray, exact: np.ndarray) -> n
     g = K * u / (1.0 - K * u) if K > 0 else 0.0
     S = np.abs(widen_bf16(dy_bits)).T @ np.abs(widen_bf16(x_bits))
     return 2.0 ** -8 * (np.abs(exact) + g * S) + g * S + 2.0 ** -133
+
+
+def wgrad_accumulate_exact(old_bits: np.ndarray, dy_bits: np.ndarray,
+                           x_bits: np.ndarray) -> np.ndarray:
+    """Gradient accumulation over micro-batches: the stored bf16 gradient
+    plus this micro-batch's dW = dy^T x, in float64 (exact for the operand
+    sizes used here, as in wgrad_exact)."""
+    return widen_bf16(old_bits) + wgrad_exact(dy_bits, x_bits)
+
+
+def error_bound_accumulate(old_bits: np.ndarray, dy_bits: np.ndarray, x_bits: np.ndarray,
+                           exact: np.ndarray) -> np.ndarray:
+    """Elementwise bound on |q - exact| for q = bf16(fp32(old + a)), a the
+    fp32 accumulation of the product P: with |a - P| <= g S (as in
+    error_bound), z = fp32(old + a) is within 2^-24 |old + a| of old + a, and
+    bf16(z) within 2^-8 |z| of z (a full bf16 unit, twice the RNE bound, as
+    in error_bound), so with |old + a| <= |exact| + g S:
+    |q - exact| <= g S + (|exact| + g S) (2^-8 (1 + 2^-24) + 2^-24)
+               <  g S + (|exact| + g S) (2^-8 + 2^-22), plus 2^-133 for bf16
+    underflow."""
+    K = np.asarray(dy_bits).shape[0]
+    u = 2.0 ** -23
+    g = K * u / (1.0 - K * u) if K > 0 else 0.0
+    S = np.abs(widen_bf16(dy_bits)).T @ np.abs(widen_bf16(x_bits))
+    return g * S + (np.abs(exact) + g * S) * (2.0 ** -8 + 2.0 ** -22) + 2.0 ** -133
 
 
 def unit_norm(dw_bits: np.ndarray) -> float:

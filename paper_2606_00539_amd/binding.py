@@ -58,7 +58,8 @@ class gnmr_act_segment(ctypes.Structure):
 class gnmr_wgrad_problem(ctypes.Structure):
     _fields_ = [("dy", ctypes.c_void_p), ("x", ctypes.c_void_p), ("dw", ctypes.c_void_p),
                 ("tokens", ctypes.c_int64), ("out_features", ctypes.c_int32),
-                ("in_features", ctypes.c_int32)]
+                ("in_features", ctypes.c_int32), ("accumulate", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class gnmr_stats(ctypes.Structure):
@@ -199,9 +200,14 @@ def gnmr_wgrad_sumsq(dy, x, dw, tokens, out_features, in_features, tile_sumsq,
 
 
 def gnmr_wgrad_sumsq_batched(problems, tile_sumsq, stream=None) -> None:
-    """problems: iterable of (dy, x, dw, tokens, out_features, in_features)."""
-    ps = [gnmr_wgrad_problem(_dptr(a), _dptr(b), _dptr(c), int(t), int(o), int(i))
-          for a, b, c, t, o, i in problems]
+    """problems: iterable of (dy, x, dw, tokens, out_features, in_features)
+    or (dy, x, dw, tokens, out_features, in_features, accumulate)."""
+    ps = []
+    for p in problems:
+        a, b, c, t, o, i = p[:6]
+        acc = int(p[6]) if len(p) > 6 else 0
+        ps.append(gnmr_wgrad_problem(_dptr(a), _dptr(b), _dptr(c), int(t), int(o), int(i), acc,
+                                     0))
     arr = (gnmr_wgrad_problem * max(len(ps), 1))(*ps)
     _check(load_library().gnmr_wgrad_sumsq_batched(arr, len(ps), _dptr(tile_sumsq),
                                                    _stream(stream)))

@@ -112,7 +112,7 @@ struct WgProblem {
   int64_t K;
   int32_t M, N, tiles_m, tiles_n;
   int32_t tile_begin;  // first tile of this problem in the launch's tile order
-  int32_t pad;
+  int32_t accumulate;  // 1: add the product to the stored dw
 };
 
 struct WgBatch {

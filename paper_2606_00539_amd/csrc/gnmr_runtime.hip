@@ -548,6 +548,8 @@ gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t
       return fail(GNMR_E_INVALID, "dy, x and dw must be 16-byte aligned");
     if (gnmr::wgrad_tiles(q.out_features, q.in_features) > int64_t(INT32_MAX / 2))
       return fail(GNMR_E_INVALID, "too many output tiles");
+    if (q.accumulate != 0 && q.accumulate != 1)
+      return fail(GNMR_E_INVALID, "accumulate must be 0 or 1");
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   int64_t base = 0;  // first partial of the current launch
@@ -569,6 +571,7 @@ gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t
       P.tiles_m = (q.out_features + gnmr::kWgBM - 1) / gnmr::kWgBM;
       P.tiles_n = (q.in_features + gnmr::kWgBN - 1) / gnmr::kWgBN;
       P.tile_begin = int32_t(tiles);
+      P.accumulate = q.accumulate;
       tiles += t;
       ++i;
     }
@@ -583,7 +586,7 @@ gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t to
                              int32_t out_features, int32_t in_features, float* tile_sumsq,
                              void* stream) {
   if (tile_sumsq == nullptr) return fail(GNMR_E_INVALID, "tile_sumsq must be a device pointer");
-  const gnmr_wgrad_problem q{dy, x, dw, tokens, out_features, in_features};
+  const gnmr_wgrad_problem q{dy, x, dw, tokens, out_features, in_features, 0, 0};
   return gnmr_wgrad_sumsq_batched(&q, 1, tile_sumsq, stream);
 }
 

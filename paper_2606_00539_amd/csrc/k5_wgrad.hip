@@ -6,6 +6,7 @@
 // to compute from what the producer already holds, Sec. 3.1).
 //
 //   dw[o][i] = bf16_rne( sum_t dy[t][o] * x[t][i] )   fp32 accumulation
+//   (accumulating problems: bf16_rne( fp32(dw_old[o][i] + that sum) ))
 //   tile_ss[tile] = sum over the tile of float(dw)^2  fp32, fixed order
 //
 // dy: [tokens][out] bf16, x: [tokens][in] bf16, dw: [out][in] bf16, all
@@ -28,6 +29,8 @@
 // that the reads of the next buffer overlap it.  x is the matrix cores' A
 // operand, so the four accumulator rows a lane holds per group are four
 // consecutive output columns: each lane stores 8 contiguous bytes.
+#include <type_traits>
+
 #include "gnmr_internal.h"
 
 namespace gnmr {
@@ -240,34 +243,51 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
 
   // Epilogue: accumulator register r of block (i, j) holds output row
   // m = m0 + 128*wm + 32*i + lane%32 and column
-  // n = n0 + 128*wn + 32*j + 8*(r/4) + 4*(lane/32) + r%4.
+  // n = n0 + 128*wn + 32*j + 8*(r/4) + 4*(lane/32) + r%4.  When the problem
+  // accumulates, the stored gradient is first widened and added in fp32 (one
+  // rounding), then the sum is rounded to bf16 once.
   float ss = 0.0f;
   const int m_lane = m0 + wm * 128 + (lane & 31);
   const int n_lane = n0 + wn * 128 + 4 * (lane >> 5);
+  auto epilogue = [&](auto accumulate) {
+    constexpr bool kAcc = decltype(accumulate)::value;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m_lane + 32 * i;
+    for (int i = 0; i < 4; ++i) {
+      const int m = m_lane + 32 * i;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 4; ++j) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = n_lane + 32 * j + 8 * g;
-        const uint32_t b0 = to_bf16(acc[i][j][4 * g + 0]);
-        const uint32_t b1 = to_bf16(acc[i][j][4 * g + 1]);
-        const uint32_t b2 = to_bf16(acc[i][j][4 * g + 2]);
-        const uint32_t b3 = to_bf16(acc[i][j][4 * g + 3]);
-        if (m < M && n < N) {
-          const float q0 = bf16_val(b0), q1 = bf16_val(b1), q2 = bf16_val(b2),
-                      q3 = bf16_val(b3);
-          ss = fmaf(q0, q0, ss);
-          ss = fmaf(q1, q1, ss);
-          ss = fmaf(q2, q2, ss);
-          ss = fmaf(q3, q3, ss);
-          *(g_vec2*)(dw + int64_t(m) * N + n) = u32x2{b0 | (b1 << 16), b2 | (b3 << 16)};
+        for (int g = 0; g < 4; ++g) {
+          const int n = n_lane + 32 * j + 8 * g;
+          if (m < M && n < N) {
+            g_vec2* dst = (g_vec2*)(dw + int64_t(m) * N + n);
+            float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1],
+                  v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+            if constexpr (kAcc) {
+              const u32x2 old = *dst;
+              v0 += bf16_val(old.x & 0xFFFFu);
+              v1 += bf16_val(old.x >> 16);
+              v2 += bf16_val(old.y & 0xFFFFu);
+              v3 += bf16_val(old.y >> 16);
+            }
+            const uint32_t b0 = to_bf16(v0), b1 = to_bf16(v1), b2 = to_bf16(v2),
+                           b3 = to_bf16(v3);
+            const float q0 = bf16_val(b0), q1 = bf16_val(b1), q2 = bf16_val(b2),
+                        q3 = bf16_val(b3);
+            ss = fmaf(q0, q0, ss);
+            ss = fmaf(q1, q1, ss);
+            ss = fmaf(q2, q2, ss);
+            ss = fmaf(q3, q3, ss);
+            *dst = u32x2{b0 | (b1 << 16), b2 | (b3 << 16)};
+          }
         }
       }
     }
-  }
+  };
+  if (P.accumulate != 0)
+    epilogue(std::integral_constant<bool, true>{});
+  else
+    epilogue(std::integral_constant<bool, false>{});
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) ss += __shfl_xor(ss, d, 64);
   if (lane == 0) red[wave] = ss;

@@ -110,8 +110,11 @@ def _fused_linear_function():
             def backward(ctx, dy):
                 x, weight = ctx.saved_tensors
                 dx = torch.matmul(dy, weight) if ctx.needs_input_grad[0] else None
-                dw = ctx.units._weight_grad(ctx.index, dy, x) if ctx.needs_input_grad[1] else None
-                return dx, dw, None, None
+                if ctx.needs_input_grad[1]:
+                    # K5 writes (or accumulates into) weight.grad itself, so
+                    # autograd receives no weight gradient to accumulate
+                    ctx.units._weight_grad(ctx.index, weight, dy, x)
+                return dx, None, None, None
 
         _FUNCTION = FusedWgradLinear
     return _FUNCTION
@@ -131,17 +134,20 @@ def _kernel_operand(t, features: int):
 class FusedWgradUnits:
     """Bias-free or biased bf16 `torch.nn.Linear` layers as GNMR units whose
     norms come from the weight-gradient GEMM itself (K5, the sum of squares
-    in its epilogue): each layer's forward is routed through an autograd
-    function whose backward computes dW = dy^T x with gnmr_wgrad_sumsq into a
-    fresh tensor that becomes `weight.grad`, and writes the layer's tile
-    partials; `step()` then runs the controller from those partials
-    (gnmr_step_from_partials), so the gradients are never re-read for their
-    norms.  Only the weight is the unit; a bias gradient is computed by torch.
+    in its epilogue).  Each layer's forward is routed through an autograd
+    function whose backward computes dx with torch and dW = dy^T x with
+    gnmr_wgrad_sumsq_batched straight into `weight.grad`: into a new tensor
+    when `weight.grad` is None, otherwise accumulated into the existing one
+    (gradient accumulation over micro-batches, as torch would accumulate),
+    and writes the layer's tile partials of the stored gradient.  `step()`
+    then runs the controller from those partials (gnmr_step_from_partials),
+    so the gradients are never re-read for their norms.  Only the weight is
+    the unit; a bias gradient is computed by torch.
 
-    Each layer must run forward exactly once per step, and `weight.grad` must
-    be None before backward (zero_grad(set_to_none=True)): if autograd
-    accumulated into an existing gradient, the partials would describe only
-    the last product, and `step()` raises instead.
+    The weight gradient does not pass through autograd's accumulation, so
+    hooks registered on the weights' gradient accumulation do not run.
+    `step()` raises if a layer did not run since the last step or if
+    `weight.grad` was replaced since its backward.
     """
 
     def __init__(self, named_linears, window: int = 5, max_o: int = 8, lock_len: int = 8,
@@ -176,7 +182,7 @@ class FusedWgradUnits:
         self.ctl = Controller(U, window, max_o, lock_len, eps, np.zeros(U + 1, np.int64), [], [],
                               None, rec, stream, budget_mode, warmup_steps)
         self.ctl.bind_partials(self.part_off)
-        self._produced = [None] * U   # data pointer of each layer's dW this step
+        self._produced = [None] * U   # data pointer of each layer's weight.grad
         self._saved_forward = []
         for b, m in enumerate(self.modules):
             self._saved_forward.append(m.__dict__.get("forward"))
@@ -190,21 +196,30 @@ class FusedWgradUnits:
             return y if m.bias is None else y + m.bias
         return forward
 
-    def _weight_grad(self, b, dy, x):
+    def _weight_grad(self, b, weight, dy, x):
         import torch
 
-        from .binding import gnmr_wgrad_sumsq
+        from .binding import gnmr_wgrad_sumsq_batched
 
         o, i = self.shapes[b]
         if dy.dtype != torch.bfloat16 or x.dtype != torch.bfloat16:
             raise TypeError(f"{self.unit_names[b]}: activations and gradients must be bf16")
         dy2, x2 = _kernel_operand(dy, o), _kernel_operand(x, i)
-        dw = torch.empty((o, i), dtype=torch.bfloat16, device=dy.device)
+        g = weight.grad
+        if g is None:
+            g = torch.empty((o, i), dtype=torch.bfloat16, device=dy.device)
+            accumulate = 0
+        else:
+            if g.dtype != torch.bfloat16 or not g.is_contiguous() or g.data_ptr() % 16:
+                raise RuntimeError(f"{self.unit_names[b]}: an existing weight.grad must be a "
+                                   "contiguous, 16-byte-aligned bf16 tensor")
+            accumulate = 1
         lo, hi = int(self.part_off[b]), int(self.part_off[b + 1])
-        gnmr_wgrad_sumsq(dy2, x2, dw, dy2.shape[0], o, i, self.partials[lo:hi],
-                         torch.cuda.current_stream())
-        self._produced[b] = dw.data_ptr()
-        return dw
+        gnmr_wgrad_sumsq_batched([(dy2, x2, g, dy2.shape[0], o, i, accumulate)],
+                                 self.partials[lo:hi], torch.cuda.current_stream())
+        if accumulate == 0:
+            weight.grad = g
+        self._produced[b] = g.data_ptr()
 
     def step(self, alpha_t: float, beta_t: float, stream=None) -> None:
         """One controller step from this backward's tile partials (asynchronous)."""
@@ -213,8 +228,7 @@ class FusedWgradUnits:
             if self._produced[b] is None or g is None or g.data_ptr() != self._produced[b]:
                 raise RuntimeError(
                     f"{self.unit_names[b]}: weight.grad is not the gradient the fused backward "
-                    "produced this step (layer unused, or accumulated into an existing grad; "
-                    "call zero_grad(set_to_none=True) before backward)")
+                    "wrote since the last step (the layer did not run, or .grad was replaced)")
         self.ctl.step_from_partials(self.partials, alpha_t, beta_t, stream)
         self._produced = [None] * len(self.modules)
 

@@ -40,7 +40,7 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(B.gnmr_config) == 40
     assert ctypes.sizeof(B.gnmr_segments) == 40
     assert ctypes.sizeof(B.gnmr_stats) == 40
-    assert ctypes.sizeof(B.gnmr_wgrad_problem) == 40
+    assert ctypes.sizeof(B.gnmr_wgrad_problem) == 48
 
 
 @pytest.mark.parametrize("bad", [

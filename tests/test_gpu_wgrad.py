@@ -339,8 +339,9 @@ def _block_forward(m, x, q_gain=1.0):
 def test_fused_wgrad_units_in_autograd_match_torch_and_k1():
     """FusedWgradUnits routes a model's linear layers through K5 in backward:
     the weight gradients agree with torch's own backward within two bf16
-    roundings, and the controller step from the tile partials makes the same
-    decisions as the K1 step (TorchUnits) over the same stored gradients."""
+    roundings, the controller step from the tile partials makes the same
+    decisions as the K1 step (TorchUnits) over the same stored gradients, and
+    a second micro-batch accumulates into the stored gradients."""
     import copy
 
     torch = require_gpu()
@@ -384,10 +385,24 @@ def test_fused_wgrad_units_in_autograd_match_torch_and_k1():
             assert_step_matches(out_k, ref, rtol=1e-5, what=f"k1 t={t}")
             if t == 6:
                 assert out_f["mask"][0] == 1, "the q spike must send q to the recovery path"
-        # accumulating into an existing gradient is refused, not silently wrong
-        y = _block_forward(fused_m, x)
-        y.float().square().mean().backward()
-        with pytest.raises(RuntimeError, match="zero_grad"):
+        # gradient accumulation: a second micro-batch before the step adds to
+        # the stored gradients in place, as torch's own backward would, and
+        # the step's norms are those of the accumulated gradients
+        x2 = torch.randn(136, 256, generator=g).to("cuda", torch.bfloat16)
+        for model in (fused_m, ref_m):
+            _block_forward(model, x2).float().square().mean().backward()
+        for n in fused_m:
+            a = fused_m[n].weight.grad.float()
+            b = ref_m[n].weight.grad.float()
+            tol = 2.0 ** -6 * b.abs() + 2e-3 * b.abs().max()
+            assert bool(((a - b).abs() <= tol).all()), f"accumulated {n}: dW differs from torch"
+        fused.step(1.1, 1.5)
+        out_f = fused.query()
+        norms = np.array([W.unit_norm(fused_m[n].weight.grad.view(torch.int16).cpu().numpy()
+                                      .view(np.uint16)) for n in fused_m])
+        np.testing.assert_allclose(out_f["norm"], norms, rtol=SS_RTOL, atol=0)
+        # a layer that did not run since the last step is refused, not stale
+        with pytest.raises(RuntimeError, match="did not run"):
             fused.step(1.1, 1.5)
     finally:
         fused.close()
@@ -460,3 +475,57 @@ def test_fused_layer_step_captured_in_a_graph_replays_like_eager():
                 assert np.array_equal(oe[k], og[k]), f"t={t}: {k}"
             assert oe["stats"] == og["stats"], f"t={t}: stats"
         assert og["stats"]["t"] == steps
+
+
+@pytest.mark.parametrize("M,N,T", [(264, 520, 70), (1032, 264, 200), (8, 8, 1)])
+def test_accumulate_integer_operands_bit_exact(M, N, T):
+    """accumulate = 1 on integer data whose sums stay exact: the stored
+    gradient becomes bf16(old + dy^T x) bit for bit, tile sums of the result."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    say(f"wgrad accumulate integer M={M} N={N} T={T}")
+    dy, x = SW.small_integer_operands(M + 3 * N + T, T, M, N, vmax=1)
+    rng = np.random.default_rng(M * N)
+    old = W.bf16_rne(rng.integers(-8, 9, size=(M, N)).astype(np.float64))
+    dw = to_dev(torch, old)
+    ss = torch.full((gnmr_wgrad_num_tiles(M, N),), float("nan"), device="cuda")
+    gnmr_wgrad_sumsq_batched([(to_dev(torch, dy), to_dev(torch, x), dw, T, M, N, 1)], ss)
+    torch.cuda.synchronize()
+    got = dw.cpu().numpy().view(np.uint16)
+    want = W.bf16_rne(W.wgrad_accumulate_exact(old, dy, x))
+    assert np.array_equal(got, want)
+    np.testing.assert_allclose(ss.cpu().numpy(), W.tile_sumsq(want), rtol=SS_RTOL, atol=0)
+
+
+def test_accumulate_random_operands_within_bound_and_mixed_batch():
+    """Random operands: accumulated gradients inside error_bound_accumulate,
+    tile sums of exactly what was stored; in one batched launch next to a
+    non-accumulating problem, which still overwrites."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    shapes = [(576, 776, 1000), (264, 520, 300)]
+    ops = [SW.operands(4, 1, b, tokens=T, out_f=M, in_f=N) for b, (M, N, T) in enumerate(shapes)]
+    olds = [W.bf16_rne(W.wgrad_exact(*SW.operands(4, 2, b, tokens=T, out_f=M, in_f=N)))
+            for b, (M, N, T) in enumerate(shapes)]
+    dws = [to_dev(torch, o) for o in olds]
+    tiles = [gnmr_wgrad_num_tiles(M, N) for M, N, _ in shapes]
+    off = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    ss = torch.full((int(off[-1]),), float("nan"), device="cuda")
+    gnmr_wgrad_sumsq_batched([(to_dev(torch, dy), to_dev(torch, x), dws[b], T, M, N, 1 - b)
+                              for b, ((dy, x), (M, N, T)) in enumerate(zip(ops, shapes))], ss)
+    torch.cuda.synchronize()
+    ss = ss.cpu().numpy()
+    for b, ((dy, x), (M, N, T)) in enumerate(zip(ops, shapes)):
+        got = dws[b].cpu().numpy().view(np.uint16)
+        if b == 0:
+            exact = W.wgrad_accumulate_exact(olds[b], dy, x)
+            bound = W.error_bound_accumulate(olds[b], dy, x, exact)
+        else:
+            exact = W.wgrad_exact(dy, x)
+            bound = W.error_bound(dy, x, exact)
+        bad = np.argwhere(np.abs(W.widen_bf16(got) - exact) > bound)
+        assert bad.size == 0, f"problem {b}: outside the bound at {bad[:8].tolist()}"
+        np.testing.assert_allclose(ss[off[b]:off[b + 1]], W.tile_sumsq(got), rtol=SS_RTOL,
+                                   atol=0, err_msg=f"problem {b}")

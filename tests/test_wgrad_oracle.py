@@ -160,3 +160,36 @@ def test_llama_layer_shapes():
     assert L.num_units == 7
     assert L.flops == 2 * 4096 * (4 * 5120 * 5120 + 3 * 13824 * 5120)
     assert L.grad_bytes == 2 * (4 * 5120 * 5120 + 3 * 13824 * 5120)
+
+
+@pytest.mark.parametrize("order", ["forward", "shuffled"])
+def test_accumulate_bound_covers_fp32_add_then_bf16(order):
+    # a stored bf16 gradient plus an fp32 accumulation, added in fp32 and
+    # rounded to bf16 once: inside error_bound_accumulate
+    dy, x = SW.operands(0, 1, 2, tokens=384, out_f=24, in_f=40, dy_scale=1e-3)
+    old_dy, old_x = SW.operands(0, 2, 2, tokens=384, out_f=24, in_f=40, dy_scale=1e-3)
+    old = W.bf16_rne(W.wgrad_exact(old_dy, old_x))
+    K = dy.shape[0]
+    idx = np.arange(K) if order == "forward" else np.random.default_rng(5).permutation(K)
+    acc = _fp32_accumulate(dy, x, idx)
+    z = (W.widen_bf16(old).astype(np.float32) + acc).astype(np.float32)
+    q = W.widen_bf16(W.bf16_rne(z.astype(np.float64)))
+    exact = W.wgrad_accumulate_exact(old, dy, x)
+    assert np.all(np.abs(q - exact) <= W.error_bound_accumulate(old, dy, x, exact))
+
+
+def test_accumulate_exact_is_old_plus_product():
+    dy, x = SW.small_integer_operands(8, tokens=6, out_f=4, in_f=5, vmax=2)
+    old = W.bf16_rne(np.arange(20, dtype=np.float64).reshape(4, 5) - 7.0)
+    got = W.wgrad_accumulate_exact(old, dy, x)
+    assert np.array_equal(got, (np.arange(20).reshape(4, 5) - 7.0) + W.wgrad_exact(dy, x))
+
+
+def test_accumulate_bound_is_violated_by_a_dropped_old_gradient():
+    # a kernel that overwrites instead of accumulating falls outside the bound
+    dy, x = SW.operands(0, 1, 3, tokens=128, out_f=16, in_f=16, dy_scale=1e-3)
+    old = W.bf16_rne(W.wgrad_exact(*SW.operands(0, 3, 3, tokens=128, out_f=16, in_f=16,
+                                                dy_scale=1e-3)))
+    exact = W.wgrad_accumulate_exact(old, dy, x)
+    q = W.widen_bf16(W.bf16_rne(W.wgrad_exact(dy, x)))
+    assert np.any(np.abs(q - exact) > W.error_bound_accumulate(old, dy, x, exact))
