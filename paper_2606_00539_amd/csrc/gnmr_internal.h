@@ -74,10 +74,12 @@ struct SelectArgs {
   gnmr_stats* stats;
 };
 
-// K4 (actuator): one workgroup per token row; up to kK4Vpt 16-byte vectors
-// per lane, so rows of at most kK4Block * kK4Vpt * 8 bf16 features.
+// K4 (actuator): up to kK4Vpt 16-byte vectors per lane; one wavefront per
+// row of at most kK4WaveCols bf16 features, one workgroup per longer row of
+// at most kK4MaxCols.
 constexpr int kK4Block = 256;
 constexpr int kK4Vpt = 8;
+constexpr int kK4WaveCols = 64 * kK4Vpt * 8;
 constexpr int kK4MaxCols = kK4Block * kK4Vpt * 8;
 
 struct ActSeg {
@@ -123,8 +125,11 @@ struct WgBatch {
 
 int64_t wgrad_tiles(int32_t M, int32_t N);
 hipError_t launch_wgrad(const WgBatch& batch, hipStream_t s);
-hipError_t launch_actuate(const RowItem* items, int64_t num_rows, const ActSeg* segs,
-                          const uint8_t* mask, int fmt_low, int fmt_rec, hipStream_t s);
+// Rows [0, num_narrow) of `items` have at most kK4WaveCols features (one
+// wavefront each), rows [num_narrow, num_rows) more (one workgroup each).
+hipError_t launch_actuate(const RowItem* items, int64_t num_narrow, int64_t num_rows,
+                          const ActSeg* segs, const uint8_t* mask, int fmt_low, int fmt_rec,
+                          hipStream_t s);
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,
                         const int32_t* seg_dtype, float* partial, hipStream_t s);
 hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,

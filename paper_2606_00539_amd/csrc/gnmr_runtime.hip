@@ -762,6 +762,7 @@ struct gnmr_actuator {
   int device = 0;
   int32_t num_units = 0;
   int64_t rows = 0;
+  int64_t narrow_rows = 0;  // rows [0, narrow_rows) of the list take one wavefront each
   int64_t bytes = 0;
   void* arena = nullptr;
   gnmr::RowItem* d_items = nullptr;
@@ -793,19 +794,26 @@ gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* se
     bytes += g.rows * int64_t(g.cols) * 2;
   }
   if (rows > int64_t(UINT32_MAX)) return fail(GNMR_E_INVALID, "too many rows in total");
+  // Row list: the rows that one wavefront handles first, then the longer ones.
   std::vector<gnmr::RowItem> items;
   items.reserve(size_t(rows));
   std::vector<gnmr::ActSeg> dsegs(static_cast<size_t>(num_segments));
-  for (int64_t k = 0; k < num_segments; ++k) {
+  for (int64_t k = 0; k < num_segments; ++k)
     dsegs[size_t(k)] = gnmr::ActSeg{static_cast<const char*>(segs[k].in),
                                     static_cast<char*>(segs[k].out), segs[k].cols, segs[k].unit};
-    for (int64_t r = 0; r < segs[k].rows; ++r)
-      items.push_back(gnmr::RowItem{int32_t(k), int32_t(r)});
-  }
+  for (int pass = 0; pass < 2; ++pass)
+    for (int64_t k = 0; k < num_segments; ++k)
+      if ((segs[k].cols <= gnmr::kK4WaveCols) == (pass == 0))
+        for (int64_t r = 0; r < segs[k].rows; ++r)
+          items.push_back(gnmr::RowItem{int32_t(k), int32_t(r)});
+  int64_t narrow = 0;
+  for (int64_t k = 0; k < num_segments; ++k)
+    if (segs[k].cols <= gnmr::kK4WaveCols) narrow += segs[k].rows;
   gnmr_actuator* a = new (std::nothrow) gnmr_actuator;
   if (a == nullptr) return fail(GNMR_E_NOMEM, "host allocation failed");
   a->num_units = num_units;
   a->rows = rows;
+  a->narrow_rows = narrow;
   a->bytes = bytes;
   const size_t o_items = 0;
   const size_t o_segs = align_up(std::max<size_t>(items.size() * sizeof(gnmr::RowItem), 1), 256);
@@ -844,8 +852,8 @@ gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_
     return fail(GNMR_E_INVALID, "unknown format");
   DeviceGuard g(act->device);
   if (!g.ok) return fail(GNMR_E_HIP, "cannot select the actuator's device");
-  GNMR_HIP(gnmr::launch_actuate(act->d_items, act->rows, act->d_segs, d_mask, fmt_low,
-                                fmt_recovery, static_cast<hipStream_t>(stream)));
+  GNMR_HIP(gnmr::launch_actuate(act->d_items, act->narrow_rows, act->rows, act->d_segs, d_mask,
+                                fmt_low, fmt_recovery, static_cast<hipStream_t>(stream)));
   return GNMR_OK;
 }
 

@@ -4,11 +4,14 @@
 // format's representable range, rounded to the nearest representable value
 // and rescaled; Sec. 5.1 / App. E.4: token-wise low-bit saved activations).
 //
-// One workgroup per token row (up to 16384 features, held in registers):
-// amax by a max-reduction, one fp32 division each for the scale and its
-// reciprocal, then per element y = x * inv, round to the format (ties to the
-// even significand, saturating), out = bf16_rne(q * s).  A row whose unit
-// takes the BF16 path in place is left untouched without reading it.
+// One wavefront per token row of up to 4096 features, one workgroup per
+// longer row (up to 16384), the row held in registers: amax by a
+// max-reduction, one fp32 division each for the scale and its reciprocal,
+// then per element y = x * inv, round to the format (ties to the even
+// significand, saturating), out = bf16_rne(q * s).  A row whose unit takes
+// the BF16 path in place is left untouched without reading it.  Rows are
+// dealt to the eight XCDs in contiguous runs, and both loads and stores are
+// non-temporal: every byte is read and written once.
 #include "gnmr_internal.h"
 
 namespace gnmr {
@@ -37,9 +40,13 @@ __device__ __forceinline__ Format format_of(int fmt) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-__device__ __forceinline__ uint32_t to_bf16(float x) {
-  uint32_t u = __float_as_uint(x);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to packed bf16, round to nearest even (one
+// v_cvt_pk_bf16_f32; the values here are finite).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // Nearest representable value of the format to y, ties to the even
@@ -58,18 +65,23 @@ __device__ __forceinline__ float round_to_format(float y, const Format& f) {
 __device__ __forceinline__ uint32_t quant_pair(uint32_t w, float inv, float s, const Format& f) {
   const float lo = __fmul_rn(round_to_format(__fmul_rn(bf16_lo(w), inv), f), s);
   const float hi = __fmul_rn(round_to_format(__fmul_rn(bf16_hi(w), inv), f), s);
-  return to_bf16(lo) | (to_bf16(hi) << 16);
+  return pack_bf16(lo, hi);
 }
 
 __device__ __forceinline__ float max_abs_pair(uint32_t w, float m) {
   return fmaxf(m, fmaxf(fabsf(bf16_lo(w)), fabsf(bf16_hi(w))));
 }
 
-__global__ __launch_bounds__(kK4Block) void k4_actuate(const RowItem* __restrict__ items,
-                                                       const ActSeg* __restrict__ segs,
-                                                       const uint8_t* __restrict__ mask,
-                                                       int fmt_low, int fmt_rec) {
-  const RowItem it = items[blockIdx.x];
+__device__ __forceinline__ void store(g_vec* p, const u32x4& v) {
+  __builtin_nontemporal_store(v, p);
+}
+
+// One row by LANES lanes (64: a wavefront; kK4Block: the workgroup).  Every
+// lane of the group calls it; `red` is workgroup LDS when LANES > 64.
+template <int LANES>
+__device__ __forceinline__ void actuate_row(const RowItem it, const ActSeg* __restrict__ segs,
+                                            const uint8_t* __restrict__ mask, int fmt_low,
+                                            int fmt_rec, int lane, float* red) {
   const ActSeg sg = segs[it.seg];
   const int fmt = mask[sg.unit] ? fmt_rec : fmt_low;
   const int64_t row_off = int64_t(it.row) * sg.cols * 2;
@@ -77,19 +89,18 @@ __global__ __launch_bounds__(kK4Block) void k4_actuate(const RowItem* __restrict
   const g_cvec* in = (const g_cvec*)(sg.in + row_off);
   g_vec* out = (g_vec*)(sg.out + row_off);
   const int nvec = sg.cols >> 3;
-  const int tid = threadIdx.x;
 
   u32x4 v[kK4Vpt];
 #pragma unroll
   for (int k = 0; k < kK4Vpt; ++k) {
-    const int i = tid + k * kK4Block;
+    const int i = lane + k * LANES;
     v[k] = i < nvec ? __builtin_nontemporal_load(in + i) : u32x4{0u, 0u, 0u, 0u};
   }
   if (fmt == GNMR_FMT_BF16) {  // BF16 path out of place: a copy
 #pragma unroll
     for (int k = 0; k < kK4Vpt; ++k) {
-      const int i = tid + k * kK4Block;
-      if (i < nvec) out[i] = v[k];
+      const int i = lane + k * LANES;
+      if (i < nvec) store(out + i, v[k]);
     }
     return;
   }
@@ -105,17 +116,20 @@ __global__ __launch_bounds__(kK4Block) void k4_actuate(const RowItem* __restrict
   }
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
-  __shared__ float red[kK4Block / 64];
-  if ((tid & 63) == 0) red[tid >> 6] = m;
-  __syncthreads();
-  const float amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float amax = m;
+  if constexpr (LANES > 64) {
+    static_assert(LANES == 4 * 64, "four waves per row");
+    if ((lane & 63) == 0) red[lane >> 6] = m;
+    __syncthreads();
+    amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  }
 
   const Format f = format_of(fmt);
   if (amax == 0.0f) {  // an all-zero token stays zero
 #pragma unroll
     for (int k = 0; k < kK4Vpt; ++k) {
-      const int i = tid + k * kK4Block;
-      if (i < nvec) out[i] = u32x4{0u, 0u, 0u, 0u};
+      const int i = lane + k * LANES;
+      if (i < nvec) store(out + i, u32x4{0u, 0u, 0u, 0u});
     }
     return;
   }
@@ -123,25 +137,56 @@ __global__ __launch_bounds__(kK4Block) void k4_actuate(const RowItem* __restrict
   const float s = __fdiv_rn(amax, f.fmax);    // and back
 #pragma unroll
   for (int k = 0; k < kK4Vpt; ++k) {
-    const int i = tid + k * kK4Block;
+    const int i = lane + k * LANES;
     if (i < nvec) {
       u32x4 o;
       o.x = quant_pair(v[k].x, inv, s, f);
       o.y = quant_pair(v[k].y, inv, s, f);
       o.z = quant_pair(v[k].z, inv, s, f);
       o.w = quant_pair(v[k].w, inv, s, f);
-      out[i] = o;
+      store(out + i, o);
     }
   }
 }
 
+// Workgroup w runs on XCD w % 8: give each XCD a contiguous run of [0, n).
+__device__ __forceinline__ uint32_t xcd_order(uint32_t w, uint32_t n) {
+  const uint32_t x = w % kNumXcd, j = w / kNumXcd, q = n / kNumXcd, r = n % kNumXcd;
+  return x * q + (x < r ? x : r) + j;
+}
+
+// At most 80 VGPRs (six waves per SIMD): more rows in flight per CU.
+__global__ __launch_bounds__(kK4Block) __attribute__((amdgpu_waves_per_eu(6, 8))) void
+k4_actuate_wave(const RowItem* __restrict__ items, uint32_t num_rows,
+                const ActSeg* __restrict__ segs, const uint8_t* __restrict__ mask, int fmt_low,
+                int fmt_rec) {
+  const uint32_t rows_per_wg = kK4Block / 64;
+  const uint32_t r = xcd_order(blockIdx.x, gridDim.x) * rows_per_wg + (threadIdx.x >> 6);
+  if (r >= num_rows) return;
+  actuate_row<64>(items[r], segs, mask, fmt_low, fmt_rec, int(threadIdx.x & 63), nullptr);
+}
+
+__global__ __launch_bounds__(kK4Block) __attribute__((amdgpu_waves_per_eu(6, 8))) void
+k4_actuate(const RowItem* __restrict__ items, const ActSeg* __restrict__ segs,
+           const uint8_t* __restrict__ mask, int fmt_low, int fmt_rec) {
+  __shared__ float red[kK4Block / 64];
+  const RowItem it = items[xcd_order(blockIdx.x, gridDim.x)];
+  actuate_row<kK4Block>(it, segs, mask, fmt_low, fmt_rec, int(threadIdx.x), red);
+}
+
 }  // namespace
 
-hipError_t launch_actuate(const RowItem* items, int64_t num_rows, const ActSeg* segs,
-                          const uint8_t* mask, int fmt_low, int fmt_rec, hipStream_t s) {
-  if (num_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k4_actuate, dim3(unsigned(num_rows)), dim3(kK4Block), 0, s, items, segs,
-                     mask, fmt_low, fmt_rec);
+hipError_t launch_actuate(const RowItem* items, int64_t num_narrow, int64_t num_rows,
+                          const ActSeg* segs, const uint8_t* mask, int fmt_low, int fmt_rec,
+                          hipStream_t s) {
+  const int64_t rows_per_wg = kK4Block / 64;
+  if (num_narrow > 0)
+    hipLaunchKernelGGL(k4_actuate_wave, dim3(unsigned((num_narrow + rows_per_wg - 1) / rows_per_wg)),
+                       dim3(kK4Block), 0, s, items, uint32_t(num_narrow), segs, mask, fmt_low,
+                       fmt_rec);
+  if (num_rows > num_narrow)
+    hipLaunchKernelGGL(k4_actuate, dim3(unsigned(num_rows - num_narrow)), dim3(kK4Block), 0, s,
+                       items + num_narrow, segs, mask, fmt_low, fmt_rec);
   return hipGetLastError();
 }
 
