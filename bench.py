@@ -250,6 +250,24 @@ def actuator_bench(torch, tokens: int, steps: int, warmup: int) -> None:
         results[label] = {"ms": round(ms, 4), "bytes_moved": moved,
                           "GBs": round(moved / (ms * 1e-3) / 1e9, 1)}
     a = results["all_low_cost"]
+    # the read-and-write reference on the same bytes: a plain non-temporal copy
+    from synth.gpu import ReadProbe
+
+    rp = ReadProbe()
+    dst = torch.empty_like(buf)
+    nb = buf.numel() * 2 // 16 * 16
+    for _ in range(2):
+        rp.copy(buf.data_ptr(), dst.data_ptr(), nb)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(5):
+        rp.copy(buf.data_ptr(), dst.data_ptr(), nb)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_ms = e0.elapsed_time(e1) / 5
+    copy_gbs = 2 * nb / (copy_ms * 1e-3) / 1e9
+    del dst
     print(json.dumps({
         "metric": "recovery actuator GB/s (bf16 read + write, per-token E2M1 fake quantisation)",
         "value": a["GBs"], "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
@@ -259,7 +277,10 @@ def actuator_bench(torch, tokens: int, steps: int, warmup: int) -> None:
                    "tokens": tokens, "activation_bytes": nbytes},
         "roofline": {"bound": "hbm", "achieved": a["GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(a["GBs"] / HBM_PEAK_GBS, 4), "kernel": "k4_actuate",
-                     "algorithmic_bytes": a["bytes_moved"]},
+                     "algorithmic_bytes": a["bytes_moved"],
+                     "frac_of_copy_probe": round(a["GBs"] / copy_gbs, 4)},
+        "copy_probe": {"kind": "plain non-temporal copy of the same bytes (read + write)",
+                       "ms": round(copy_ms, 4), "GBs": round(copy_gbs, 1)},
         "cases": results}), flush=True)
     act.close()
 

@@ -199,3 +199,56 @@ int synth_read_probe(const void* p, int64_t bytes, float* partials, int32_t vari
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Read-and-write reference: a plain copy of `bytes` (a multiple of 16) from
+// src to dst, 4 non-temporal 16-byte loads then 4 non-temporal stores per
+// lane, one 16 KiB block per workgroup in XCD-contiguous order (the best of
+// a sweep of block sizes on this part).  A reference point for kernels that
+// read and write every byte once.
+// ---------------------------------------------------------------------------
+namespace {
+
+typedef __attribute__((address_space(1))) u32x4 g_vec_w;
+constexpr int kCopyUnroll = 4;
+constexpr int64_t kCopyBlockVecs = int64_t(kBlock) * kCopyUnroll;
+
+__global__ __launch_bounds__(kBlock) void probe_copy(const g_vec* __restrict__ src,
+                                                     g_vec_w* __restrict__ dst, int64_t nvec) {
+  const uint32_t nblk = gridDim.x, w = blockIdx.x;
+  const uint32_t x = w % 8, j = w / 8, q = nblk / 8, r = nblk % 8;
+  const int64_t v0 = (int64_t(x) * q + (x < r ? x : r) + j) * kCopyBlockVecs;
+  u32x4 v[kCopyUnroll];
+#pragma unroll
+  for (int k = 0; k < kCopyUnroll; ++k) {
+    const int64_t i = v0 + threadIdx.x + int64_t(k) * kBlock;
+    if (i < nvec) v[k] = __builtin_nontemporal_load(src + i);
+  }
+#pragma unroll
+  for (int k = 0; k < kCopyUnroll; ++k) {
+    const int64_t i = v0 + threadIdx.x + int64_t(k) * kBlock;
+    if (i < nvec) __builtin_nontemporal_store(v[k], dst + i);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Launches one copy on `stream`; both addresses 16-byte aligned, the ranges
+// disjoint.  Returns 0 or a hipError_t (1 = hipErrorInvalidValue).
+int synth_copy_probe(const void* src, void* dst, int64_t bytes, void* stream) {
+  if (src == nullptr || dst == nullptr || bytes <= 0 || bytes % 16 != 0 ||
+      (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 16 != 0)
+    return int(hipErrorInvalidValue);
+  const int64_t nvec = bytes / 16;
+  const int64_t grid = (nvec + kCopyBlockVecs - 1) / kCopyBlockVecs;
+  if (grid > int64_t(UINT32_MAX)) return int(hipErrorInvalidValue);
+  hipLaunchKernelGGL(probe_copy, dim3(unsigned(grid)), dim3(kBlock), 0,
+                     static_cast<hipStream_t>(stream),
+                     (const g_vec*)reinterpret_cast<uintptr_t>(src),
+                     (g_vec_w*)reinterpret_cast<uintptr_t>(dst), nvec);
+  return int(hipGetLastError());
+}
+
+}  // extern "C"

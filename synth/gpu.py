@@ -58,7 +58,8 @@ class Generator:
 class ReadProbe:
     """Plain read-reduce kernels over a contiguous device buffer (the
     benchmark's read-ceiling reference points): variant 0 is a grid-stride
-    loop, variant 1 one 64 KiB block per workgroup in XCD-contiguous order."""
+    loop, variant 1 one 64 KiB block per workgroup in XCD-contiguous order;
+    and a plain copy, the read-and-write reference."""
 
     VARIANTS = {0: "grid_stride_nt", 1: "blocked_nt_xcd"}
 
@@ -71,6 +72,9 @@ class ReadProbe:
         self.lib.synth_read_probe.restype = ctypes.c_int
         self.lib.synth_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                               ctypes.c_int32, ctypes.c_void_p]
+        self.lib.synth_copy_probe.restype = ctypes.c_int
+        self.lib.synth_copy_probe.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                              ctypes.c_void_p]
 
     def num_partials(self, nbytes: int, variant: int) -> int:
         return int(self.lib.synth_read_probe_partials(int(nbytes), int(variant)))
@@ -79,3 +83,9 @@ class ReadProbe:
         rc = self.lib.synth_read_probe(ptr, int(nbytes), partials_ptr, int(variant), stream)
         if rc != 0:
             raise RuntimeError(f"synth_read_probe failed with hipError {rc}")
+
+    def copy(self, src_ptr: int, dst_ptr: int, nbytes: int, stream: int = 0):
+        """The read-and-write reference: a plain non-temporal copy."""
+        rc = self.lib.synth_copy_probe(src_ptr, dst_ptr, int(nbytes), stream)
+        if rc != 0:
+            raise RuntimeError(f"synth_copy_probe failed with hipError {rc}")

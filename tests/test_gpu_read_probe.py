@@ -38,3 +38,17 @@ def test_read_probe_rejects_bad_arguments():
                       (buf.data_ptr(), 64, 2), (0, 64, 0)]:
         with pytest.raises(RuntimeError):
             rp.run(ptr, n, parts.data_ptr(), v)
+
+
+@pytest.mark.parametrize("nvec", [1, 1023, 1024, 1025, 3_000_017])
+def test_copy_probe_copies_exactly(nvec):
+    torch = require_gpu()
+    from synth.gpu import ReadProbe
+
+    rp = ReadProbe()
+    src = torch.arange(nvec * 4, dtype=torch.int32, device="cuda")
+    dst = torch.full((nvec * 4 + 64,), -1, dtype=torch.int32, device="cuda")
+    rp.copy(src.data_ptr(), dst.data_ptr(), nvec * 16)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:nvec * 4], src)
+    assert bool((dst[nvec * 4:] == -1).all()), "copied past the end"
