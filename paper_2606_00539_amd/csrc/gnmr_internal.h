@@ -136,5 +136,9 @@ hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,
                              int64_t num_items, int32_t num_units, double* out, hipStream_t s);
 hipError_t launch_update(const UpdateArgs& a, int64_t num_items, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+// K2 and K3 as one single-workgroup launch: used when the workload is small
+// (at most 1024 units, each summed by one thread, or norms given).
+bool single_launch_update_select(const UpdateArgs& a, int64_t num_items);
+hipError_t launch_update_select(const UpdateArgs& u, const SelectArgs& s, hipStream_t st);
 
 }  // namespace gnmr

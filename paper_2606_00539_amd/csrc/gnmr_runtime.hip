@@ -215,12 +215,21 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, const float* 
   s.lock = c->d_lock;
   s.mask = c->d_mask;
   s.stats = c->d_stats;
-  GNMR_HIP(gnmr::launch_update(u, num_parts, st));
-  gnmr_status r = record(c, 2, st);
-  if (r != GNMR_OK) return r;
-  GNMR_HIP(gnmr::launch_select(s, st));
-  r = record(c, 3, st);
-  if (r != GNMR_OK) return r;
+  gnmr_status r = GNMR_OK;
+  if (gnmr::single_launch_update_select(u, num_parts)) {
+    // small workload: K2 + K3 in one launch (timed as the update; select 0)
+    GNMR_HIP(gnmr::launch_update_select(u, s, st));
+    r = record(c, 2, st);
+    if (r == GNMR_OK) r = record(c, 3, st);
+    if (r != GNMR_OK) return r;
+  } else {
+    GNMR_HIP(gnmr::launch_update(u, num_parts, st));
+    r = record(c, 2, st);
+    if (r != GNMR_OK) return r;
+    GNMR_HIP(gnmr::launch_select(s, st));
+    r = record(c, 3, st);
+    if (r != GNMR_OK) return r;
+  }
   if (c->prof && c->prof_steps < kProfileCapacity) ++c->prof_steps;
   return GNMR_OK;
 }
@@ -750,7 +759,12 @@ gnmr_status gnmr_info(const gnmr_ctx* ctx, int64_t* num_items, int64_t* item_byt
   if (num_items) *num_items = ctx->num_items;
   if (item_bytes) *item_bytes = gnmr::kItemBytes;
   if (bytes_per_step) *bytes_per_step = ctx->bytes_per_step;
-  if (launches_per_step) *launches_per_step = ctx->num_items > 0 ? 3 : 2;
+  if (launches_per_step) {
+    gnmr::UpdateArgs u{};
+    u.num_units = ctx->U;
+    *launches_per_step = (ctx->num_items > 0 ? 1 : 0) +
+                         (gnmr::single_launch_update_select(u, ctx->num_items) ? 1 : 2);
+  }
   return GNMR_OK;
 }
 

@@ -410,6 +410,23 @@ __device__ void select_body(const SelectArgs& a) {
 
 __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) { select_body(a); }
 
+// K2 and K3 in one workgroup, for small workloads: at most kK3Block units,
+// each summed by one thread exactly as k2_update<1> sums it (or given its
+// norm), then the selection of K3 after a workgroup barrier, which makes
+// K2's keys, flags, candidate list and counters visible to every thread.
+// One launch instead of two; the same arithmetic, so the same results.
+__global__ __launch_bounds__(kK3Block) void k23_small(UpdateArgs u, SelectArgs s) {
+  const int b = int(threadIdx.x);
+  if (b < u.num_units) {
+    const double n = u.ext_norm != nullptr
+                         ? u.ext_norm[b]
+                         : sqrt(unit_ss<1>(u.unit_item_off, u.partial, b, 0, nullptr));
+    update_unit<true>(u, b, n);
+  }
+  __syncthreads();
+  select_body(s);
+}
+
 }  // namespace
 
 // Lanes per unit for the partial sums: one thread when units have few items,
@@ -451,6 +468,16 @@ hipError_t launch_update(const UpdateArgs& a, int64_t num_items, hipStream_t s) 
     hipLaunchKernelGGL(k2_update<64>, unit_grid<64>(a.num_units), dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL(k2_update<256>, unit_grid<256>(a.num_units), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+bool single_launch_update_select(const UpdateArgs& a, int64_t num_items) {
+  return a.num_units <= kK3Block &&
+         (a.ext_norm != nullptr || lanes_per_unit(num_items, a.num_units) == 1);
+}
+
+hipError_t launch_update_select(const UpdateArgs& u, const SelectArgs& s, hipStream_t st) {
+  hipLaunchKernelGGL(k23_small, dim3(1), dim3(kK3Block), 0, st, u, s);
   return hipGetLastError();
 }
 

@@ -90,6 +90,9 @@ def test_fullsize_sampled(gen, name, steps):
     pool = ThreadPoolExecutor(max_workers=min(8, len(sample)))
     try:
         with controller_for(lay, w, ptrs) as ctl:
+            # K1, K2, K3: every full-size workload is too large for the
+            # single-workgroup K2 + K3 launch
+            assert ctl.info()["launches_per_step"] == 3
             for t in range(1, steps + 1):
                 alpha, beta = w.alpha(t), w.beta(t)
                 s32 = w.scale32(t)
