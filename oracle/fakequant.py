@@ -9,7 +9,7 @@ nearest representable value, and rescaled to the original range.  The format
 is chosen per unit by the controller's mask: the low-cost format when the unit
 is on the low-cost path, the recovery format when it is in A_t.
 
-Readings (also in DESIGN.md):
+Readings:
   * formats are the OCP 8-bit and MX sub-byte floating-point formats without
     inf/NaN: E2M1 (max 6), E3M2 (max 28), E4M3 (max 448), E5M2 (max 57344);
     format 0 is the identity (the BF16 path);

@@ -27,7 +27,7 @@ What it computes, per controller step t = 1, 2, ... (paper notation):
   locks   b in A_t and R > 1 -> Lock_b = T_lock; b in A_t and R <= 1 ->
           Lock_b = max(Lock_b - 1, 0); b not in A_t -> Lock_b = 0 (Alg. 2).
 
-Readings where the paper is silent (each also listed in the design doc):
+Readings where the paper is silent:
   * Ties in Top_maxO are broken by the smaller unit index.
   * eps = 0 with a zero D-GNMR denominator gives D-GNMR = 1 (the same
     convention Alg. 1 uses for A = 0).

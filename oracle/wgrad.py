@@ -12,7 +12,7 @@ controller sees is the norm of the stored bf16 values; it is split here into
 the sums of squares over the 256x256 tiles of dW, in row-major tile order,
 which is the unit of work of the fused kernel.
 
-Readings (also in DESIGN.md):
+Readings:
   * stored gradient = bf16 round-to-nearest-even of the product;
   * the exact product is the float64 matrix product of the exactly widened
     bf16 operands; for the operand sizes used here (at most a few thousand
