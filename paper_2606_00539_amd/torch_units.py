@@ -101,10 +101,12 @@ def _fused_linear_function():
 
         class FusedWgradLinear(torch.autograd.Function):
             @staticmethod
-            def forward(ctx, x, weight, units, index):
+            def forward(ctx, x, weight, bias, units, index):
                 ctx.save_for_backward(x, weight)
                 ctx.units, ctx.index = units, index
-                return torch.matmul(x, weight.t())
+                ctx.has_bias = bias is not None
+                # the same product as nn.Linear (bias fused: one rounding)
+                return torch.nn.functional.linear(x, weight, bias)
 
             @staticmethod
             def backward(ctx, dy):
@@ -114,7 +116,10 @@ def _fused_linear_function():
                     # K5 writes (or accumulates into) weight.grad itself, so
                     # autograd receives no weight gradient to accumulate
                     ctx.units._weight_grad(ctx.index, weight, dy, x)
-                return dx, None, None, None
+                db = None
+                if ctx.has_bias and ctx.needs_input_grad[2]:
+                    db = dy.reshape(-1, dy.shape[-1]).sum(0)
+                return dx, None, db, None, None
 
         _FUNCTION = FusedWgradLinear
     return _FUNCTION
@@ -141,8 +146,9 @@ class FusedWgradUnits:
     (gradient accumulation over micro-batches, as torch would accumulate),
     and writes the layer's tile partials of the stored gradient.  `step()`
     then runs the controller from those partials (gnmr_step_from_partials),
-    so the gradients are never re-read for their norms.  Only the weight is
-    the unit; a bias gradient is computed by torch.
+    so the gradients are never re-read for their norms.  The forward is
+    nn.Linear's (bias fused into the product); only the weight is the unit,
+    and a bias gradient is the sum of dy over the tokens.
 
     The weight gradient does not pass through autograd's accumulation, so
     hooks registered on the weights' gradient accumulation do not run.
@@ -192,8 +198,7 @@ class FusedWgradUnits:
         fn = _fused_linear_function()
 
         def forward(x):
-            y = fn.apply(x, m.weight, self, b)
-            return y if m.bias is None else y + m.bias
+            return fn.apply(x, m.weight, m.bias, self, b)
         return forward
 
     def _weight_grad(self, b, weight, dy, x):

@@ -388,7 +388,8 @@ def test_fused_wgrad_units_in_autograd_match_torch_and_k1():
         # gradient accumulation: a second micro-batch before the step adds to
         # the stored gradients in place, as torch's own backward would, and
         # the step's norms are those of the accumulated gradients
-        x2 = torch.randn(136, 256, generator=g).to("cuda", torch.bfloat16)
+        # (a [batch, sequence, features] micro-batch: 2 x 68 tokens)
+        x2 = torch.randn(2, 68, 256, generator=g).to("cuda", torch.bfloat16)
         for model in (fused_m, ref_m):
             _block_forward(model, x2).float().square().mean().backward()
         for n in fused_m:
@@ -529,3 +530,45 @@ def test_accumulate_random_operands_within_bound_and_mixed_batch():
         assert bad.size == 0, f"problem {b}: outside the bound at {bad[:8].tolist()}"
         np.testing.assert_allclose(ss[off[b]:off[b + 1]], W.tile_sumsq(got), rtol=SS_RTOL,
                                    atol=0, err_msg=f"problem {b}")
+
+
+def test_fused_wgrad_units_with_bias_and_unaligned_views():
+    """A biased layer (bias gradient left to torch) fed a view that starts off
+    a 16-byte boundary: the operand is copied to an aligned buffer, and dW,
+    dx, the bias gradient and the step's norm match torch and the stored
+    gradient."""
+    import copy
+
+    torch = require_gpu()
+    from paper_2606_00539_amd.torch_units import FusedWgradUnits
+
+    g = torch.Generator(device="cpu").manual_seed(9)
+    lin = torch.nn.Linear(264, 136, bias=True)
+    with torch.no_grad():
+        lin.weight.copy_(torch.randn(136, 264, generator=g) * 0.05)
+        lin.bias.copy_(torch.randn(136, generator=g))
+    lin = lin.to("cuda", torch.bfloat16)
+    ref = copy.deepcopy(lin)
+    fused = FusedWgradUnits([("lin", lin)], max_o=1, lock_len=1)
+    try:
+        base = torch.randn(40 * 264 + 3, generator=g).to("cuda", torch.bfloat16)
+        x = base[3:].view(40, 264)                     # 6 bytes past an aligned start
+        assert x.data_ptr() % 16 != 0
+        xa = x.detach().clone().requires_grad_(True)
+        xb = x.detach().clone().requires_grad_(True)
+        ya, yb = lin(xa), ref(xb)
+        assert torch.equal(ya, yb), "the routed forward must be nn.Linear's"
+        ya.float().square().sum().backward()
+        yb.float().square().sum().backward()
+        a, b = lin.weight.grad.float(), ref.weight.grad.float()
+        assert bool(((a - b).abs() <= 2.0 ** -7 * b.abs() + 1e-3 * b.abs().max()).all())
+        ga, gb = lin.bias.grad.float(), ref.bias.grad.float()
+        assert bool(((ga - gb).abs() <= 2.0 ** -7 * gb.abs() + 1e-3 * gb.abs().max()).all())
+        dxa, dxb = xa.grad.float(), xb.grad.float()
+        assert bool(((dxa - dxb).abs() <= 2.0 ** -7 * dxb.abs() + 1e-3 * dxb.abs().max()).all())
+        fused.step(1.5, 1.5)
+        norm = fused.query()["norm"][0]
+        want = W.unit_norm(lin.weight.grad.view(torch.int16).cpu().numpy().view(np.uint16))
+        np.testing.assert_allclose(norm, want, rtol=SS_RTOL, atol=0)
+    finally:
+        fused.close()
