@@ -257,10 +257,10 @@ gnmr_status gnmr_info(const gnmr_ctx* ctx, int64_t* num_items, int64_t* item_byt
  * the recovery path chosen by the controller (Alg. 2: "use the recovery path
  * for b" / "use the low-cost path").  Both paths are per-token fake
  * quantisation (App. E.2 quantisation-simulated operators; Sec. 5.1 and App.
- * E.4: token-wise low-bit saved activations): every token (row) is scaled into
+ * E.4: token-wise low-bit saved activations; Sec. 5.3 and App. E.3: INT8): every token (row) is scaled into
  * the format's representable range by its largest magnitude, rounded to the
- * nearest representable value (ties to the even significand, saturating) and
- * rescaled, in fp32: inv = fmax / amax, s = amax / fmax, y = x * inv,
+ * nearest representable value (ties to the even significand or integer,
+ * saturating) and rescaled, in fp32: inv = fmax / amax, s = amax / fmax, y = x * inv,
  * out = bf16_rne(round(y) * s), signs kept; an all-zero token becomes +0.
  * GNMR_FMT_BF16 leaves the row unchanged.
  * ------------------------------------------------------------------------- */
@@ -269,7 +269,9 @@ enum {
   GNMR_FMT_E2M1 = 1,  /* 4-bit, max 6                                  */
   GNMR_FMT_E3M2 = 2,  /* 6-bit, max 28                                 */
   GNMR_FMT_E4M3 = 3,  /* 8-bit, max 448                                */
-  GNMR_FMT_E5M2 = 4   /* 8-bit, max 57344                              */
+  GNMR_FMT_E5M2 = 4,  /* 8-bit, max 57344                              */
+  GNMR_FMT_INT8 = 5   /* symmetric integer grid -127 .. 127 (Sec. 5.3, App.
+                         E.3: the INT8 low-cost path); rint, ties to even  */
 };
 
 /* One unit's saved activations: a row-major bf16 [rows][cols] matrix, one

@@ -2,7 +2,8 @@
 activations -- TEST INFRASTRUCTURE ONLY (same rules as the rest of oracle/).
 
 What it computes (App. E.2, quantisation-simulated operators; Sec. 5.1 and
-App. E.4, token-wise low-bit quantisation of saved activations): for each
+App. E.4, token-wise low-bit quantisation of saved activations; the INT8
+low-cost path of the LLaMA-2 13B fine-tuning test, Sec. 5.3 and App. E.3): for each
 token (one row of a unit's [tokens, features] activation matrix), the values
 are scaled into the representable range of the target format, rounded to the
 nearest representable value, and rescaled to the original range.  The format
@@ -13,6 +14,10 @@ Readings:
   * formats are the OCP 8-bit and MX sub-byte floating-point formats without
     inf/NaN: E2M1 (max 6), E3M2 (max 28), E4M3 (max 448), E5M2 (max 57344);
     format 0 is the identity (the BF16 path);
+  * INT8 (format 5) is symmetric per-token integer quantisation, the grid
+    {-127, ..., 127} (the code -128 is not used, so the grid is symmetric):
+    fmax = 127, q = rint(y) with ties to the even integer, clamped to
+    [-127, 127]; the rest of the recipe is the one of the float formats;
   * arithmetic is fp32 with round-to-nearest-even: amax = max |x| over the
     token, inv = fmax / amax and s = amax / fmax (one division each per
     token), y = x * inv, q = the representable value nearest to y (ties to
@@ -32,7 +37,14 @@ FORMATS = {
     3: (3, -6, 448.0),       # E4M3, bias 7 (no inf; S.1111.111 is NaN, so 448 is max)
     4: (2, -14, 57344.0),    # E5M2, bias 15
 }
-FORMAT_NAMES = {0: "bf16", 1: "e2m1", 2: "e3m2", 3: "e4m3", 4: "e5m2"}
+# integer format id -> largest magnitude of the symmetric grid
+INT_FORMATS = {5: 127.0}   # INT8
+FORMAT_NAMES = {0: "bf16", 1: "e2m1", 2: "e3m2", 3: "e4m3", 4: "e5m2", 5: "int8"}
+
+
+def fmax_of(fmt: int) -> float:
+    """Largest magnitude of a format's grid."""
+    return INT_FORMATS[fmt] if fmt in INT_FORMATS else FORMATS[fmt][2]
 
 
 def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -60,12 +72,21 @@ def round_to_format(y: np.ndarray, fmt: int) -> np.ndarray:
     return np.copysign(q, y).astype(np.float32)     # the sign of y is kept, -0 included
 
 
+def round_to_int(y: np.ndarray, fmt: int) -> np.ndarray:
+    """Nearest integer to each fp32 y (ties to even), clamped to the
+    symmetric grid [-qmax, qmax]; the sign of y is kept, -0 included."""
+    qmax = INT_FORMATS[fmt]
+    y = np.asarray(y, np.float32)
+    q = np.minimum(np.rint(np.abs(y).astype(np.float64)), qmax)
+    return np.copysign(q, y).astype(np.float32)
+
+
 def fakequant_rows(x_bits: np.ndarray, fmt: int) -> np.ndarray:
     """Fake-quantise every row of a [rows, cols] bf16 matrix (uint16 bits)."""
     x_bits = np.asarray(x_bits, np.uint16)
     if fmt == 0:
         return x_bits.copy()
-    _, _, fmax = FORMATS[fmt]
+    fmax = fmax_of(fmt)
     x = bf16_to_f32(x_bits)
     amax = np.max(np.abs(x), axis=1, keepdims=True).astype(np.float32)
     nz = amax > 0
@@ -73,7 +94,7 @@ def fakequant_rows(x_bits: np.ndarray, fmt: int) -> np.ndarray:
     inv = (np.float32(fmax) / safe).astype(np.float32)        # fp32 division, RNE
     s = (safe / np.float32(fmax)).astype(np.float32)          # fp32 division, RNE
     y = (x * inv).astype(np.float32)                           # fp32 product, RNE
-    q = round_to_format(y, fmt)
+    q = round_to_int(y, fmt) if fmt in INT_FORMATS else round_to_format(y, fmt)
     out = (q * s).astype(np.float32)                           # fp32 product, RNE
     out = np.where(nz, out, np.float32(0.0))
     return f32_to_bf16(out)

@@ -21,7 +21,8 @@ GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED, GNMR_BUDGET_STATIC = 0, 1, 2
 STATUS_NAMES = {0: "GNMR_OK", -1: "GNMR_E_INVALID", -2: "GNMR_E_NOMEM", -3: "GNMR_E_HIP",
                 -4: "GNMR_E_STATE"}
 
-GNMR_FMT_BF16, GNMR_FMT_E2M1, GNMR_FMT_E3M2, GNMR_FMT_E4M3, GNMR_FMT_E5M2 = 0, 1, 2, 3, 4
+GNMR_FMT_BF16, GNMR_FMT_E2M1, GNMR_FMT_E3M2, GNMR_FMT_E4M3, GNMR_FMT_E5M2, GNMR_FMT_INT8 = \
+    0, 1, 2, 3, 4, 5
 
 EXPORTED = ("gnmr_init", "gnmr_destroy", "gnmr_step", "gnmr_step_from_norms", "gnmr_sumsq",
             "gnmr_query", "gnmr_device_outputs", "gnmr_state_size", "gnmr_get_state",

@@ -861,8 +861,8 @@ gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* se
 gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_low,
                          int32_t fmt_recovery, void* stream) {
   if (act == nullptr || d_mask == nullptr) return fail(GNMR_E_INVALID, "NULL argument");
-  if (fmt_low < GNMR_FMT_BF16 || fmt_low > GNMR_FMT_E5M2 || fmt_recovery < GNMR_FMT_BF16 ||
-      fmt_recovery > GNMR_FMT_E5M2)
+  if (fmt_low < GNMR_FMT_BF16 || fmt_low > GNMR_FMT_INT8 || fmt_recovery < GNMR_FMT_BF16 ||
+      fmt_recovery > GNMR_FMT_INT8)
     return fail(GNMR_E_INVALID, "unknown format");
   DeviceGuard g(act->device);
   if (!g.ok) return fail(GNMR_E_HIP, "cannot select the actuator's device");

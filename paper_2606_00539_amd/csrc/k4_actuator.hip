@@ -2,7 +2,8 @@
 // of saved activations, the format chosen per unit by the controller's mask
 // (App. E.2 quantisation-simulated operators: each token is scaled into the
 // format's representable range, rounded to the nearest representable value
-// and rescaled; Sec. 5.1 / App. E.4: token-wise low-bit saved activations).
+// and rescaled; Sec. 5.1 / App. E.4: token-wise low-bit saved activations;
+// Sec. 5.3 / App. E.3: the INT8 low-cost path).
 //
 // One wavefront per token row of up to 4096 features, one workgroup per
 // longer row (up to 16384), the row held in registers: amax by a
@@ -28,8 +29,12 @@ struct Format {
 };
 
 // E2M1, E3M2, E4M3 (OCP, 448 max), E5M2 (57344 max); no inf/NaN produced.
+// The symmetric INT8 grid {0, 1, ..., 127} is the same rounding with the
+// lowest binade at 2^6 and 6 fraction bits: a step of 1 below 128 and
+// saturation at 127.
 __device__ __forceinline__ Format format_of(int fmt) {
   switch (fmt) {
+    case GNMR_FMT_INT8: return Format{6, 6, 127.0f};
     case GNMR_FMT_E2M1: return Format{1, 0, 6.0f};
     case GNMR_FMT_E3M2: return Format{2, -2, 28.0f};
     case GNMR_FMT_E4M3: return Format{3, -6, 448.0f};

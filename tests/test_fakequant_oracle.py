@@ -102,6 +102,82 @@ def test_fakequant_rows_properties(fmt):
     assert np.array_equal(FQ.bf16_to_f32(out2), of * np.float32(2.0 ** 5))
 
 
+def test_int8_round_is_nearest_integer():
+    """INT8: brute force over the 255-value grid, ties to the even integer,
+    saturation at +-127, signs (and -0) kept."""
+    g = np.arange(0, 128, dtype=np.float64)
+    rng = np.random.default_rng(55)
+    y = np.concatenate([rng.uniform(-140, 140, 20000), rng.uniform(-2, 2, 2000),
+                        np.concatenate([g, -g, g[:-1] + 0.5, -(g[:-1] + 0.5)]),
+                        [127.49, 127.5, 127.51, 128.0, 1e6, -1e6, 0.0, -0.0, 1e-40]]
+                       ).astype(np.float32)
+    got = FQ.round_to_int(y, 5).astype(np.float64)
+    a = np.abs(y).astype(np.float64)
+    d = np.abs(a[:, None] - g[None, :])
+    best = d.min(axis=1)
+    cand = d == best[:, None]
+    # among equidistant grid values take the even one (an integer tie)
+    pick = np.where(cand.sum(axis=1) > 1, np.argmax(cand & (g[None, :] % 2 == 0), axis=1),
+                    np.argmax(cand, axis=1))
+    want = np.copysign(g[pick], y)
+    assert np.array_equal(got, want)
+    assert np.array_equal(np.signbit(got), np.signbit(y))
+    assert FQ.round_to_int(np.float32([2.5, 3.5, -2.5, 126.5]), 5).tolist() == [2, 4, -2, 126]
+
+
+def test_int8_rows():
+    """INT8 per-token rows: every output is an integer multiple of amax/127
+    (up to the final bf16 rounding), the largest element returns to amax, and
+    the quantisation error of each element is at most half a step."""
+    rng = np.random.default_rng(56)
+    x = rng.normal(size=(17, 300)).astype(np.float32) * 10.0 ** rng.uniform(-5, 3, (17, 1))
+    x[4] = 0.0
+    x[4, ::3] = -0.0                                           # an all-zero token with -0s
+    x[6, 9] = -800.0
+    xb = FQ.f32_to_bf16(x)
+    out = FQ.fakequant_rows(xb, 5)
+    xf, of = FQ.bf16_to_f32(xb).astype(np.float64), FQ.bf16_to_f32(out).astype(np.float64)
+    assert np.all(of[4] == 0) and not np.any(np.signbit(of[4]))
+    for r in range(x.shape[0]):
+        amax = np.abs(xf[r]).max()
+        if amax == 0:
+            continue
+        s = amax / 127.0
+        k = np.rint(of[r] / s)
+        assert np.all(np.abs(k) <= 127)
+        # bf16 keeps 8 significant bits: within 2^-8 of k s (plus fp32 slack)
+        assert np.all(np.abs(of[r] - k * s) <= 2.0 ** -8 * np.abs(k * s) + 1e-6 * s)
+        assert np.all(np.abs(xf[r] - k * s) <= 0.5 * s * (1 + 1e-5))
+        assert abs(np.abs(of[r]).max() - amax) <= 2.0 ** -8 * amax
+        assert np.array_equal(np.signbit(of[r]), np.signbit(xf[r]))
+    # the integer grid: INT8 of data already on a grid of amax/127 is exact
+    grid_rows = (np.arange(-127, 128, dtype=np.float32) * np.float32(2.0 ** -3))[None, :]
+    exact = FQ.fakequant_rows(FQ.f32_to_bf16(grid_rows), 5)
+    assert np.array_equal(FQ.bf16_to_f32(exact), grid_rows)
+
+
+def test_f32_to_bf16_is_nearest_even():
+    """fp32 -> bf16 against the two neighbouring bf16 values in float64:
+    the nearer one, the one with the even last bit at an exact tie."""
+    rng = np.random.default_rng(57)
+    u = rng.integers(0, 0x7F7F0000, 50000, dtype=np.uint32)
+    u[:64] = (rng.integers(0x00800000, 0x7F000000, 64, dtype=np.uint32) & 0xFFFF0000) | 0x8000
+    u = np.concatenate([u, u | np.uint32(0x80000000)])      # both signs
+    x = u.view(np.float32)
+    got = FQ.f32_to_bf16(x)
+    lo = (u & np.uint32(0xFFFF0000))
+    hi = lo + np.uint32(0x10000)
+    xl, xh = lo.view(np.float32).astype(np.float64), hi.view(np.float32).astype(np.float64)
+    d_lo = np.abs(x.astype(np.float64) - xl)
+    d_hi = np.abs(x.astype(np.float64) - xh)
+    lo16, hi16 = (lo >> 16).astype(np.uint16), (hi >> 16).astype(np.uint16)
+    want = np.where(d_lo < d_hi, lo16, np.where(d_hi < d_lo, hi16,
+                                                 np.where(lo16 % 2 == 0, lo16, hi16)))
+    assert np.array_equal(got, want)
+    assert FQ.f32_to_bf16(np.float32([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8])).tolist() == \
+        [0x3F80, 0x3F82]
+
+
 def test_identity_format_and_actuate():
     rng = np.random.default_rng(3)
     a = FQ.f32_to_bf16(rng.normal(size=(4, 16)).astype(np.float32))

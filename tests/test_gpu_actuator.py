@@ -30,7 +30,7 @@ def to_device(torch, a):
     return t
 
 
-@pytest.mark.parametrize("fmts", [(1, 0), (1, 3), (2, 0), (4, 2), (3, 1), (0, 0)])
+@pytest.mark.parametrize("fmts", [(1, 0), (1, 3), (2, 0), (4, 2), (3, 1), (0, 0), (5, 0), (1, 5)])
 @pytest.mark.parametrize("inplace", [False, True])
 def test_actuator_matches_oracle(fmts, inplace):
     torch = require_gpu()
@@ -81,3 +81,30 @@ def test_actuator_follows_the_controller_mask():
         got = d_in[b].cpu().numpy().view(np.uint16).reshape(16, 4096)
         want = acts[b] if mask[b] else FQ.fakequant_rows(acts[b], GNMR_FMT_E2M1)
         assert np.array_equal(got, want)
+
+
+def test_actuator_int8_ties_and_rejects_unknown_formats():
+    """INT8: a token whose amax is 127 has scale 1, so every x + 0.5 is an
+    exact tie (to the even integer); formats outside 0..5 are refused."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import GNMR_FMT_INT8, Actuator, GnmrError
+
+    k = np.arange(0, 127, dtype=np.float32)
+    row = np.concatenate([[127.0], k + 0.5, -(k + 0.5), k, [-127.0]]).astype(np.float32)
+    row = np.pad(row, (0, (-row.size) % 8))
+    x = FQ.f32_to_bf16(np.stack([row, row * np.float32(2.0 ** -20)]))
+    assert np.array_equal(FQ.bf16_to_f32(x)[0], row)          # every value exact in bf16
+    d = to_device(torch, x)
+    d_mask = torch.zeros(1, dtype=torch.uint8, device="cuda")
+    with Actuator([(d, d, 2, row.size, 0)], 1) as act:
+        for bad in (-1, GNMR_FMT_INT8 + 1):
+            with pytest.raises(GnmrError):
+                act.apply(d_mask, bad, 0)
+            with pytest.raises(GnmrError):
+                act.apply(d_mask, 0, bad)
+        act.apply(d_mask, GNMR_FMT_INT8, 0)
+        torch.cuda.synchronize()
+    got = d.cpu().numpy().view(np.uint16).reshape(x.shape)
+    assert np.array_equal(got, FQ.fakequant_rows(x, GNMR_FMT_INT8))
+    q = FQ.bf16_to_f32(got)[0][1:128]
+    assert np.array_equal(q, np.where(k % 2 == 0, k, k + 1))    # ties to even

@@ -8,10 +8,11 @@ import types
 
 import pytest
 
+import test_fakequant_oracle as FP
 import test_oracle_pins as P
 
-SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle",
-                   "gnmr_oracle.py")
+ORACLE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle")
+SRC = os.path.join(ORACLE, "gnmr_oracle.py")
 
 # (name, original text, planted mistake)
 MUTANTS = [
@@ -73,8 +74,8 @@ PINS = [
 ]
 
 
-def mutant_module(original: str, planted: str) -> types.ModuleType:
-    src = open(SRC).read()
+def mutant_module(original: str, planted: str, path: str = SRC) -> types.ModuleType:
+    src = open(path).read()
     assert original in src, f"mutation anchor not found: {original!r}"
     spec = importlib.util.spec_from_loader("oracle_mutant", loader=None)
     mod = importlib.util.module_from_spec(spec)
@@ -103,3 +104,62 @@ def test_pins_catch_planted_mistake(monkeypatch, name, original, planted):
 def test_unmutated_oracle_passes_every_listed_pin():
     for fn, kw in PINS:
         fn(**kw)
+
+
+# The actuator oracle (per-token fake quantisation) and its pins.
+FQ_MUTANTS = [
+    ("float ties away from zero", "q = np.rint(a / step) * step",
+     "q = np.floor(a / step + 0.5) * step"),
+    ("float no saturation", "q = np.minimum(q, fmax)", "q = q"),
+    ("E4M3 max 480", "3: (3, -6, 448.0)", "3: (3, -6, 480.0)"),
+    ("E2M1 subnormal binade off by one", "1: (1, 0, 6.0)", "1: (1, -1, 6.0)"),
+    ("E5M2 as E5M3", "4: (2, -14, 57344.0)", "4: (3, -14, 57344.0)"),
+    ("float sign dropped", "return np.copysign(q, y).astype(np.float32)     #",
+     "return q.astype(np.float32)     #"),
+    ("int ties away from zero", "q = np.minimum(np.rint(np.abs(y).astype(np.float64)), qmax)",
+     "q = np.minimum(np.floor(np.abs(y).astype(np.float64) + 0.5), qmax)"),
+    ("int clamp at 128", "q = np.minimum(np.rint(np.abs(y).astype(np.float64)), qmax)",
+     "q = np.minimum(np.rint(np.abs(y).astype(np.float64)), qmax + 1)"),
+    ("int grid to 128", "INT_FORMATS = {5: 127.0}", "INT_FORMATS = {5: 128.0}"),
+    ("int truncates", "q = np.minimum(np.rint(np.abs(y).astype(np.float64)), qmax)",
+     "q = np.minimum(np.trunc(np.abs(y).astype(np.float64)), qmax)"),
+    ("zero token keeps -0", "out = np.where(nz, out, np.float32(0.0))", "out = out"),
+    ("scale from the column maximum", "amax = np.max(np.abs(x), axis=1, keepdims=True)",
+     "amax = np.max(np.abs(x), axis=0, keepdims=True)"),
+    ("bf16 rounds half away", "r = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1)))",
+     "r = (u + np.uint64(0x8000))"),
+    ("bf16 truncates", "r = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1)))",
+     "r = u"),
+    ("low and recovery formats swapped", "fmt_hi if m else fmt_lo", "fmt_lo if m else fmt_hi"),
+]
+
+FQ_PINS = [fn for name, fn in sorted(vars(FP).items())
+           if name.startswith("test_") and callable(fn)]
+
+
+def run_fq_pin(fn):
+    names = fn.__code__.co_varnames[:fn.__code__.co_argcount]
+    if names == ("fmt",):
+        for fmt in (1, 2, 3, 4):
+            fn(fmt)
+    else:
+        fn()
+
+
+@pytest.mark.parametrize("name,original,planted", FQ_MUTANTS, ids=[m[0] for m in FQ_MUTANTS])
+def test_actuator_pins_catch_planted_mistake(monkeypatch, name, original, planted):
+    mod = mutant_module(original, planted, os.path.join(ORACLE, "fakequant.py"))
+    monkeypatch.setattr(FP, "FQ", mod)
+    caught = []
+    for fn in FQ_PINS:
+        try:
+            run_fq_pin(fn)
+        except (AssertionError, ValueError, IndexError, KeyError, ZeroDivisionError):
+            caught.append(fn.__name__)
+    assert caught, f"no pin fails for the planted mistake: {name}"
+
+
+def test_unmutated_actuator_oracle_passes_every_pin():
+    assert len(FQ_PINS) >= 6
+    for fn in FQ_PINS:
+        run_fq_pin(fn)
