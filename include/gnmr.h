@@ -164,9 +164,10 @@ gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
  * tokens >= 0 (0 gives dw = 0).  tile_sumsq: device float [gnmr_wgrad_num_tiles(out,
  * in)], written with the fp32 sum of float(dw)^2 over each 256x256 output
  * tile (row-major tile order, ragged edge tiles included), each in a fixed
- * order: deterministic.  The caller owns every buffer; dw must not overlap
- * dy or x.  Asynchronous on `stream`.  GNMR_E_INVALID on a bad shape,
- * pointer or alignment, GNMR_E_HIP on a launch failure. */
+ * order: deterministic.  The caller owns every buffer; dw and tile_sumsq
+ * must overlap neither each other nor dy or x (checked).  Asynchronous on
+ * `stream`.  GNMR_E_INVALID on a bad shape, pointer, alignment or overlap,
+ * GNMR_E_HIP on a launch failure. */
 int64_t gnmr_wgrad_num_tiles(int32_t out_features, int32_t in_features);
 gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t tokens,
                              int32_t out_features, int32_t in_features,
@@ -181,8 +182,10 @@ gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t to
  * micro-batches): dw = bf16_rne(fp32(dw + product)), one fp32 addition and
  * one rounding to bf16, and its tile sums are those of the accumulated dw.
  * `problems` is a host array, read before return; every check of
- * gnmr_wgrad_sumsq applies to each problem (and accumulate is 0 or 1), and
- * nothing is launched if one fails. */
+ * gnmr_wgrad_sumsq applies to each problem (and accumulate is 0 or 1,
+ * reserved 0); across the batch no dw may overlap another problem's dw, dy
+ * or x, or tile_sumsq (operands may be shared between problems: the seven
+ * projections read three inputs).  Nothing is launched if a check fails. */
 typedef struct {
   const void* dy;        /* device [tokens][out_features] bf16 */
   const void* x;         /* device [tokens][in_features] bf16  */
@@ -279,7 +282,9 @@ enum {
 typedef struct {
   const void* in;   /* device, 16-byte aligned                                  */
   void* out;        /* device, 16-byte aligned; equal to `in` (in place) or not
-                       overlapping any segment's input                           */
+                       overlapping any segment's input; no two segments' outputs
+                       overlap, and no segment's input is another's output (all
+                       checked by gnmr_actuator_create)                          */
   int64_t rows;     /* tokens, >= 0                                             */
   int32_t cols;     /* features: a multiple of 8, 8 .. 16384                     */
   int32_t unit;     /* controller unit whose mask entry picks the format, 0 .. U-1 */

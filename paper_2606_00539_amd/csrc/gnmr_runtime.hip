@@ -64,6 +64,68 @@ struct DeviceGuard {
   }
 };
 
+// A byte range [lo, hi) of device memory that buffer `id` covers.
+struct Span {
+  uintptr_t lo, hi;
+  int64_t id;
+};
+
+Span span_of(const void* p, int64_t bytes, int64_t id) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return Span{lo, lo + uintptr_t(bytes), id};
+}
+
+bool intersect(const Span& a, const Span& b) {
+  return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi;
+}
+
+// Index of a write that overlaps another write, or a read of a different id;
+// -1 when there is none.  O((W + R) log R): reads sorted by start, with the
+// two largest ends of distinct ids over every prefix.
+int64_t find_overlap(std::vector<Span> w, std::vector<Span> r) {
+  auto by_lo = [](const Span& a, const Span& b) { return a.lo < b.lo; };
+  w.erase(std::remove_if(w.begin(), w.end(), [](const Span& s) { return s.lo >= s.hi; }), w.end());
+  r.erase(std::remove_if(r.begin(), r.end(), [](const Span& s) { return s.lo >= s.hi; }), r.end());
+  std::sort(w.begin(), w.end(), by_lo);
+  uintptr_t reach = 0;
+  for (size_t k = 0; k < w.size(); ++k) {
+    if (k > 0 && w[k].lo < reach) return w[k].id;
+    reach = std::max(reach, w[k].hi);
+  }
+  std::sort(r.begin(), r.end(), by_lo);
+  struct Top2 {
+    uintptr_t hi1 = 0, hi2 = 0;
+    int64_t id1 = -1, id2 = -1;
+  };
+  std::vector<Top2> pre(r.size() + 1);
+  for (size_t k = 0; k < r.size(); ++k) {
+    Top2 t = pre[k];
+    const Span& s = r[k];
+    if (s.id == t.id1) {
+      t.hi1 = std::max(t.hi1, s.hi);
+    } else if (t.id1 < 0 || s.hi > t.hi1) {
+      t.hi2 = t.hi1;
+      t.id2 = t.id1;
+      t.hi1 = s.hi;
+      t.id1 = s.id;
+    } else if (t.id2 < 0 || s.hi > t.hi2) {
+      t.hi2 = s.hi;
+      t.id2 = s.id;
+    }
+    pre[k + 1] = t;
+  }
+  for (const Span& s : w) {
+    // reads starting before the write ends; the furthest-reaching one of another id
+    const size_t k = size_t(std::lower_bound(r.begin(), r.end(), Span{s.hi, s.hi, 0}, by_lo) -
+                            r.begin());
+    const Top2& t = pre[k];
+    const bool other1 = t.id1 >= 0 && t.id1 != s.id;
+    const uintptr_t hi = other1 ? t.hi1 : (t.id2 >= 0 ? t.hi2 : 0);
+    if ((other1 || t.id2 >= 0) && hi > s.lo) return s.id;
+  }
+  return -1;
+}
+
 }  // namespace
 
 struct gnmr_ctx {
@@ -559,6 +621,30 @@ gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t
       return fail(GNMR_E_INVALID, "too many output tiles");
     if (q.accumulate != 0 && q.accumulate != 1)
       return fail(GNMR_E_INVALID, "accumulate must be 0 or 1");
+    if (q.reserved != 0) return fail(GNMR_E_INVALID, "reserved must be 0");
+  }
+  // No write may race another access: each dw and the tile sums are disjoint
+  // from one another and from every operand of the batch.
+  {
+    std::vector<Span> w, r;
+    int64_t tiles = 0;
+    for (int32_t i = 0; i < num_problems; ++i) {
+      const gnmr_wgrad_problem& q = problems[i];
+      const Span dw = span_of(q.dw, int64_t(q.out_features) * q.in_features * 2, i);
+      const Span dy = span_of(q.dy, q.tokens * q.out_features * 2, i);
+      const Span x = span_of(q.x, q.tokens * q.in_features * 2, i);
+      if (intersect(dw, dy) || intersect(dw, x))
+        return fail(GNMR_E_INVALID, "problem " + std::to_string(i) + ": dw overlaps dy or x");
+      w.push_back(dw);
+      r.push_back(dy);
+      r.push_back(x);
+      tiles += gnmr::wgrad_tiles(q.out_features, q.in_features);
+    }
+    w.push_back(span_of(tile_sumsq, tiles * int64_t(sizeof(float)), -2));
+    if (find_overlap(w, r) != -1)
+      return fail(GNMR_E_INVALID,
+                  "a problem's dw or tile_sumsq overlaps another output or another problem's "
+                  "operands");
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
   int64_t base = 0;  // first partial of the current launch
@@ -808,6 +894,24 @@ gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* se
     bytes += g.rows * int64_t(g.cols) * 2;
   }
   if (rows > int64_t(UINT32_MAX)) return fail(GNMR_E_INVALID, "too many rows in total");
+  // A segment writes in place or into memory that no segment reads, and no
+  // two segments write the same bytes.
+  {
+    std::vector<Span> w, r;
+    for (int64_t k = 0; k < num_segments; ++k) {
+      const int64_t nb = segs[k].rows * int64_t(segs[k].cols) * 2;
+      const Span in = span_of(segs[k].in, nb, k), out = span_of(segs[k].out, nb, k);
+      if (in.lo != out.lo && intersect(in, out))
+        return fail(GNMR_E_INVALID, "activation segment " + std::to_string(k) +
+                                        ": out partly overlaps in (in place needs out == in)");
+      w.push_back(out);
+      r.push_back(in);
+    }
+    const int64_t k = find_overlap(w, r);
+    if (k != -1)
+      return fail(GNMR_E_INVALID, "activation segment " + std::to_string(k) +
+                                      ": out overlaps another segment's input or output");
+  }
   // Row list: the rows that one wavefront handles first, then the longer ones.
   std::vector<gnmr::RowItem> items;
   items.reserve(size_t(rows));

@@ -86,6 +86,72 @@ def test_actuator_rejects_bad_segments(bad):
     assert e.value.status == B.GNMR_E_INVALID
 
 
+# in [4096, 4608) out [8192, 8704) for 4 rows of 64 features; each case's
+# segments are rejected in the argument checks, before any device call
+_A = (4096, 8192, 4, 64, 0)
+
+
+@pytest.mark.parametrize("segs", [
+    [(4096, 4096 + 256, 4, 64, 0)],                      # out partly overlaps its own in
+    [_A, (8192, 12288, 4, 64, 1)],                       # reads another segment's output
+    [_A, (12288, 8192 + 256, 4, 64, 1)],                 # outputs overlap
+    [(4096, 4096, 4, 64, 0), (4096, 12288, 4, 64, 1)],   # in place over another's input
+    [(8192, 8192, 4, 64, 0), (8128, 32768, 1, 40, 1)],   # in place over the tail of an input
+    [(20480, 20480, 4, 64, 0), (12288, 16384, 4, 64, 1), (16384 + 496, 24576, 1, 8, 2)],
+])
+def test_actuator_rejects_racing_segments(segs):
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_actuator_create(segs, num_units=3)
+    assert e.value.status == B.GNMR_E_INVALID
+    assert "overlap" in B.gnmr_last_error()
+
+
+def _races(segs):
+    """Brute force over every pair: a write that meets another write, another
+    segment's input, or its own input other than exactly (in place)."""
+    span = [(i, i + r * c * 2, o, o + r * c * 2) for i, o, r, c, _ in segs if r > 0]
+    meet = lambda a0, a1, b0, b1: a0 < b1 and b0 < a1  # noqa: E731
+    for k, (i0, i1, o0, o1) in enumerate(span):
+        if o0 != i0 and meet(o0, o1, i0, i1):
+            return True
+        for j, (j0, j1, p0, p1) in enumerate(span):
+            if j != k and (meet(o0, o1, j0, j1) or meet(o0, o1, p0, p1)):
+                return True
+    return False
+
+
+def test_actuator_overlap_check_equals_brute_force():
+    # random layouts of fake addresses; a layout without a race passes the
+    # checks and fails only later, at the table allocation (no device here),
+    # or succeeds where there is one (the tables hold only the addresses)
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    rng = np.random.default_rng(77)
+    seen = {True: 0, False: 0}
+    for _ in range(400):
+        n = int(rng.integers(1, 7))
+        segs = []
+        for _ in range(n):
+            i = 4096 + 16 * int(rng.integers(0, 400))
+            o = i if rng.random() < 0.3 else 4096 + 16 * int(rng.integers(0, 400))
+            segs.append((i, o, int(rng.integers(0, 3)), 8 * int(rng.integers(1, 9)),
+                         int(rng.integers(0, 3))))
+        want = _races(segs)
+        seen[want] += 1
+        try:
+            act = B.gnmr_actuator_create(segs, num_units=3)
+        except GnmrError as e:
+            assert (e.status == B.GNMR_E_INVALID) == want, (segs, B.gnmr_last_error())
+        else:
+            assert not want, segs
+            B.gnmr_actuator_destroy(act)
+    assert seen[True] > 50 and seen[False] > 50
+
+
 def test_missing_library_fails_loudly(tmp_path):
     from paper_2606_00539_amd import binding as B
 
@@ -139,6 +205,34 @@ def test_wgrad_batched_rejects_a_bad_problem_before_launching():
     assert e.value.status == B.GNMR_E_INVALID
     with pytest.raises(GnmrError):
         B.gnmr_wgrad_sumsq_batched([good], 0)
+
+
+@pytest.mark.parametrize("probs,ss", [
+    ([(4096, 8192, 4096, 16, 64, 128)], 65536),                  # dw over its own dy
+    ([(4096, 8192, 16384, 16, 64, 128)], 16384 + 4096),          # tile sums inside dw
+    ([(4096, 8192, 16384, 16, 64, 128), (40960, 45056, 16384 + 8192, 16, 64, 128)], 65536),
+    ([(4096, 8192, 16384, 16, 64, 128), (40960, 16384 + 512, 49152, 16, 64, 128)], 65536),
+    ([(4096, 8192, 16384, 16, 64, 128), (32768, 49152, 12288 - 16, 16, 16, 128)], 65536),
+])
+def test_wgrad_batched_rejects_racing_outputs(probs, ss):
+    # outputs that overlap another buffer of the batch; checked before launching
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_wgrad_sumsq_batched(probs, ss)
+    assert e.value.status == B.GNMR_E_INVALID
+    assert "overlap" in B.gnmr_last_error()
+
+
+def test_wgrad_batched_rejects_nonzero_reserved():
+    import ctypes
+
+    from paper_2606_00539_amd import binding as B
+
+    p = B.gnmr_wgrad_problem(4096, 8192, 16384, 16, 64, 128, 0, 7)
+    st = B.load_library().gnmr_wgrad_sumsq_batched(ctypes.byref(p), 1, 32768, None)
+    assert st == B.GNMR_E_INVALID and "reserved" in B.gnmr_last_error()
 
 
 def test_fused_wgrad_units_rejects_unsupported_layers():

@@ -108,3 +108,25 @@ def test_actuator_int8_ties_and_rejects_unknown_formats():
     assert np.array_equal(got, FQ.fakequant_rows(x, GNMR_FMT_INT8))
     q = FQ.bf16_to_f32(got)[0][1:128]
     assert np.array_equal(q, np.where(k % 2 == 0, k, k + 1))    # ties to even
+
+
+def test_actuator_segments_may_share_an_input():
+    """Two units read one activation matrix out of place into two outputs
+    (shared reads are not races), one in the low-cost and one in the recovery
+    format."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import Actuator
+
+    rng = np.random.default_rng(9)
+    a = FQ.f32_to_bf16(rng.normal(size=(6, 1000)).astype(np.float32))
+    d_in = to_device(torch, a)
+    outs = [torch.full_like(d_in, 0x5555) for _ in range(2)]
+    d_mask = torch.tensor([0, 1], dtype=torch.uint8, device="cuda")
+    with Actuator([(d_in, outs[0], 6, 1000, 0), (d_in, outs[1], 6, 1000, 1)], 2) as act:
+        act.apply(d_mask, 1, 5)
+        torch.cuda.synchronize()
+    assert np.array_equal(outs[0].cpu().numpy().view(np.uint16).reshape(a.shape),
+                          FQ.fakequant_rows(a, 1))
+    assert np.array_equal(outs[1].cpu().numpy().view(np.uint16).reshape(a.shape),
+                          FQ.fakequant_rows(a, 5))
+    assert np.array_equal(d_in.cpu().numpy().view(np.uint16).reshape(a.shape), a)

@@ -174,6 +174,41 @@ def test_batched_matches_single_problem_calls(count):
         assert np.array_equal(dw1, dw) and np.array_equal(ss1, ss[off[i]:off[i + 1]])
 
 
+def test_batched_problems_may_share_operands():
+    """Four problems read one input x (as q, k and v do) and write four
+    gradients; a fifth reuses the first one's dy.  Shared reads pass the
+    overlap checks, and every result is the oracle's, bit for bit on integer
+    operands."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    T, N = 130, 264
+    outs = [264, 72, 72, 520]
+    say("wgrad batched with shared operands")
+    _, x = SW.small_integer_operands(31, T, 8, N)
+    dys = [SW.small_integer_operands(32 + i, T, M, 8)[0] for i, M in enumerate(outs)]
+    d_x = to_dev(torch, x)
+    d_dy = [to_dev(torch, d) for d in dys]
+    dws = [torch.full((M, N), 0x5555, dtype=torch.int16, device="cuda") for M in outs]
+    # problem 4 reuses problem 0's dy against a second input of its own
+    _, x2 = SW.small_integer_operands(36, T, 8, 136)
+    d_x2 = to_dev(torch, x2)
+    dw4 = torch.full((outs[0], 136), 0x5555, dtype=torch.int16, device="cuda")
+    probs = [(d_dy[i], d_x, dws[i], T, M, N) for i, M in enumerate(outs)]
+    probs.append((d_dy[0], d_x2, dw4, T, outs[0], 136))
+    tiles = [gnmr_wgrad_num_tiles(M, N) for M in outs] + [gnmr_wgrad_num_tiles(outs[0], 136)]
+    off = np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+    ss = torch.full((int(off[-1]),), float("nan"), dtype=torch.float32, device="cuda")
+    gnmr_wgrad_sumsq_batched(probs, ss)
+    torch.cuda.synchronize()
+    ss = ss.cpu().numpy()
+    wants = [W.bf16_rne(W.wgrad_exact(d, x)) for d in dys] + [W.bf16_rne(W.wgrad_exact(dys[0], x2))]
+    for i, (got, want) in enumerate(zip(dws + [dw4], wants)):
+        assert np.array_equal(got.cpu().numpy().view(np.uint16), want), f"problem {i}"
+        np.testing.assert_allclose(ss[off[i]:off[i + 1]], W.tile_sumsq(want), rtol=SS_RTOL,
+                                   atol=0, err_msg=f"problem {i}")
+
+
 def small_layer():
     return SW.WgradLayer("small-layer", ((512, 512), (512, 512), (512, 512), (512, 512),
                                          (1376, 512), (1376, 512), (512, 1376)), tokens=256)
