@@ -25,6 +25,8 @@ HBM_PEAK_GBS = 8000.0
 # the sources of the gradient-pass kernel whose HBM counters profiles/ records
 K1_SOURCES = ("k1_sumsq.hip", "k1_geometry.h")
 METRIC = "GNMR step GB/s (frac. of HBM peak) + µs/step, 13B-shaped grads, 1 GPU"
+# the controller's budget policies (gnmr_config.budget_mode)
+BUDGET_MODES = {"active": 0, "admitted": 1, "static": 2}
 
 
 def log(*a):
@@ -415,6 +417,11 @@ def main():
     ap.add_argument("--wgrad", action="store_true",
                     help="measure the gradient pass fused into the weight-gradient GEMMs of "
                          "one LLaMA-2-13B layer against library GEMMs + gnmr_step")
+    ap.add_argument("--budget-mode", choices=sorted(BUDGET_MODES), default="active",
+                    help="controller policy: the active-set cap (default), the admitted-only "
+                         "budget, or the static baseline (ranked once after the warm-up)")
+    ap.add_argument("--policy-warmup", type=int, default=None,
+                    help="high-fidelity warm-up steps of the policy (default: 0; 3 for static)")
     ap.add_argument("--tokens", type=int, default=4096)
     ap.add_argument("--probe-copy-bytes", type=float, default=0,
                     help="instead of the controller, time device-to-device copies of this "
@@ -452,8 +459,13 @@ def main():
     ptrs = [base + int(o) for o in lay.seg_byte_off]
     Generator().fill(lay, base, w.seed, 1, w.scale32(1))
     stream = torch.cuda.current_stream()
+    mode = BUDGET_MODES[args.budget_mode]
+    policy_warmup = args.policy_warmup
+    if policy_warmup is None:
+        policy_warmup = 3 if args.budget_mode == "static" else 0
     ctl = Controller(w.num_units, w.window, w.max_o, w.lock_len, w.eps, lay.unit_seg_off,
-                     lay.seg_numel, lay.seg_dtype, ptrs, stream=stream)
+                     lay.seg_numel, lay.seg_dtype, ptrs, stream=stream, budget_mode=mode,
+                     warmup_steps=policy_warmup)
     info = ctl.info()
     t = 0
     for _ in range(args.warmup):
@@ -533,6 +545,7 @@ def main():
                    "lock_len": w.lock_len, "window": w.window,
                    "work_items": info["num_items"], "item_bytes": info["item_bytes"],
                    "launches_per_step": info["launches_per_step"],
+                   "budget_mode": args.budget_mode, "policy_warmup_steps": policy_warmup,
                    "timing": ("graph replays" if args.graph else "eager steps") +
                              "; kernel times from a separate pass with per-kernel HIP events"},
         "roofline": roofline,
