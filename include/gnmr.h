@@ -305,6 +305,21 @@ gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* se
 gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_low,
                          int32_t fmt_recovery, void* stream);
 
+/* One activation matrix without a row table (the rows of one segment
+ * passed by value): the same per-token quantisation, for callers whose
+ * buffers change every call, such as the input of one linear layer inside a
+ * forward pass.  in: device bf16 [rows][cols], row-major, 16-byte aligned;
+ * out: equal to `in` (in place) or not overlapping it, 16-byte aligned; cols
+ * a multiple of 8 in [8, 16384]; 0 <= rows < 2^31; the matrix takes
+ * fmt_recovery when d_mask[unit] != 0, else fmt_low (d_mask: device bytes,
+ * e.g. the controller's mask from gnmr_device_outputs, read when the kernel
+ * runs).  Allocates nothing and launches one kernel (none when rows = 0);
+ * asynchronous on `stream`.  GNMR_E_INVALID on a bad argument, GNMR_E_HIP on
+ * a launch failure. */
+gnmr_status gnmr_actuate_matrix(const void* in, void* out, int64_t rows, int32_t cols,
+                                const uint8_t* d_mask, int32_t unit, int32_t fmt_low,
+                                int32_t fmt_recovery, void* stream);
+
 /* Rows in the work list and bf16 bytes of all segments' inputs. */
 gnmr_status gnmr_actuator_info(const gnmr_actuator* act, int64_t* rows, int64_t* bytes);
 

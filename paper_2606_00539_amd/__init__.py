@@ -8,6 +8,7 @@ the thin Python binding over that ABI.
 from .binding import (GNMR_BF16, GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED,  # noqa: F401
                       GNMR_BUDGET_STATIC, GNMR_FMT_BF16, GNMR_FMT_E2M1, GNMR_FMT_E3M2,
                       GNMR_FMT_E4M3, GNMR_FMT_E5M2, GNMR_FMT_INT8, Actuator, gnmr_actuate,
+                      gnmr_actuate_matrix,
                       gnmr_actuator_create, gnmr_actuator_destroy, gnmr_actuator_info,
                       GNMR_F32, Controller, GnmrError,
                       gnmr_destroy, gnmr_device_outputs, gnmr_get_state, gnmr_info,

@@ -29,7 +29,8 @@ EXPORTED = ("gnmr_init", "gnmr_destroy", "gnmr_step", "gnmr_step_from_norms", "g
             "gnmr_set_state", "gnmr_set_profiling", "gnmr_profile_read", "gnmr_info",
             "gnmr_last_error", "gnmr_actuator_create", "gnmr_actuate", "gnmr_actuator_info",
             "gnmr_actuator_destroy", "gnmr_wgrad_num_tiles", "gnmr_wgrad_sumsq",
-            "gnmr_bind_partials", "gnmr_step_from_partials", "gnmr_wgrad_sumsq_batched")
+            "gnmr_bind_partials", "gnmr_step_from_partials", "gnmr_wgrad_sumsq_batched",
+            "gnmr_actuate_matrix")
 
 
 class GnmrError(RuntimeError):
@@ -102,6 +103,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "gnmr_info": [P, P, P, P, P],
         "gnmr_actuator_create": [P, P, I64, I32, P],
         "gnmr_actuate": [P, P, I32, I32, P],
+        "gnmr_actuate_matrix": [P, P, I64, I32, P, I32, I32, I32, P],
         "gnmr_actuator_info": [P, P, P],
         "gnmr_actuator_destroy": [P],
         "gnmr_wgrad_sumsq": [P, P, P, I64, I32, I32, P, P],
@@ -304,6 +306,13 @@ def gnmr_actuator_create(segments, num_units, stream=None) -> ctypes.c_void_p:
 def gnmr_actuate(act, d_mask, fmt_low, fmt_recovery, stream=None) -> None:
     p = d_mask.data_ptr() if hasattr(d_mask, "data_ptr") else int(d_mask)
     _check(load_library().gnmr_actuate(act, p, int(fmt_low), int(fmt_recovery), _stream(stream)))
+
+
+def gnmr_actuate_matrix(x, out, rows, cols, d_mask, unit, fmt_low, fmt_recovery,
+                        stream=None) -> None:
+    _check(load_library().gnmr_actuate_matrix(_dptr(x), _dptr(out), int(rows), int(cols),
+                                              _dptr(d_mask), int(unit), int(fmt_low),
+                                              int(fmt_recovery), _stream(stream)))
 
 
 def gnmr_actuator_info(act) -> dict:

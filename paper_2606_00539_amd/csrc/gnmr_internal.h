@@ -130,6 +130,10 @@ hipError_t launch_wgrad(const WgBatch& batch, hipStream_t s);
 hipError_t launch_actuate(const RowItem* items, int64_t num_narrow, int64_t num_rows,
                           const ActSeg* segs, const uint8_t* mask, int fmt_low, int fmt_rec,
                           hipStream_t s);
+// One [rows][sg.cols] matrix, no row table: rows <= 4 * UINT32_MAX when
+// sg.cols <= kK4WaveCols, else rows <= UINT32_MAX (one workgroup each).
+hipError_t launch_actuate_matrix(const ActSeg& sg, int64_t rows, const uint8_t* mask,
+                                 int fmt_low, int fmt_rec, hipStream_t s);
 hipError_t launch_sumsq(const Item* items, int64_t num_items, const char* const* seg_base,
                         const int32_t* seg_dtype, float* partial, hipStream_t s);
 hipError_t launch_unit_sumsq(const int64_t* unit_item_off, const float* partial,

@@ -975,6 +975,31 @@ gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_
   return GNMR_OK;
 }
 
+gnmr_status gnmr_actuate_matrix(const void* in, void* out, int64_t rows, int32_t cols,
+                                const uint8_t* d_mask, int32_t unit, int32_t fmt_low,
+                                int32_t fmt_recovery, void* stream) {
+  if (rows < 0 || rows > INT32_MAX) return fail(GNMR_E_INVALID, "rows must be in [0, 2^31)");
+  if (cols < 8 || cols > gnmr::kK4MaxCols || cols % 8 != 0)
+    return fail(GNMR_E_INVALID, "cols must be a multiple of 8 in [8, 16384]");
+  if (unit < 0) return fail(GNMR_E_INVALID, "unit must be >= 0");
+  if (fmt_low < GNMR_FMT_BF16 || fmt_low > GNMR_FMT_INT8 || fmt_recovery < GNMR_FMT_BF16 ||
+      fmt_recovery > GNMR_FMT_INT8)
+    return fail(GNMR_E_INVALID, "unknown format");
+  if (rows == 0) return GNMR_OK;
+  if (in == nullptr || out == nullptr || d_mask == nullptr)
+    return fail(GNMR_E_INVALID, "NULL argument");
+  if (reinterpret_cast<uintptr_t>(in) % 16 || reinterpret_cast<uintptr_t>(out) % 16)
+    return fail(GNMR_E_INVALID, "in and out must be 16-byte aligned");
+  const int64_t nb = rows * int64_t(cols) * 2;
+  const Span si = span_of(in, nb, 0), so = span_of(out, nb, 0);
+  if (si.lo != so.lo && intersect(si, so))
+    return fail(GNMR_E_INVALID, "out partly overlaps in (in place needs out == in)");
+  const gnmr::ActSeg sg{static_cast<const char*>(in), static_cast<char*>(out), cols, unit};
+  GNMR_HIP(gnmr::launch_actuate_matrix(sg, rows, d_mask, fmt_low, fmt_recovery,
+                                       static_cast<hipStream_t>(stream)));
+  return GNMR_OK;
+}
+
 gnmr_status gnmr_actuator_info(const gnmr_actuator* act, int64_t* rows, int64_t* bytes) {
   if (act == nullptr) return fail(GNMR_E_INVALID, "act is NULL");
   if (rows) *rows = act->rows;

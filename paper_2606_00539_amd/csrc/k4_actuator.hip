@@ -10,7 +10,9 @@
 // max-reduction, one fp32 division each for the scale and its reciprocal,
 // then per element y = x * inv, round to the format (ties to the even
 // significand, saturating), out = bf16_rne(q * s).  A row whose unit takes
-// the BF16 path in place is left untouched without reading it.  Rows are
+// the BF16 path in place is left untouched without reading it.  The rows come
+// from a table built once over many segments (k4_actuate*), or from one
+// matrix passed by value (k4_matrix*, no table).  Rows are
 // dealt to the eight XCDs in contiguous runs, and both loads and stores are
 // non-temporal: every byte is read and written once.
 #include "gnmr_internal.h"
@@ -81,15 +83,15 @@ __device__ __forceinline__ void store(g_vec* p, const u32x4& v) {
   __builtin_nontemporal_store(v, p);
 }
 
-// One row by LANES lanes (64: a wavefront; kK4Block: the workgroup).  Every
-// lane of the group calls it; `red` is workgroup LDS when LANES > 64.
+// Row `row` of segment sg by LANES lanes (64: a wavefront; kK4Block: the
+// workgroup).  Every lane of the group calls it; `red` is workgroup LDS when
+// LANES > 64.
 template <int LANES>
-__device__ __forceinline__ void actuate_row(const RowItem it, const ActSeg* __restrict__ segs,
+__device__ __forceinline__ void actuate_row(const ActSeg sg, int64_t row,
                                             const uint8_t* __restrict__ mask, int fmt_low,
                                             int fmt_rec, int lane, float* red) {
-  const ActSeg sg = segs[it.seg];
   const int fmt = mask[sg.unit] ? fmt_rec : fmt_low;
-  const int64_t row_off = int64_t(it.row) * sg.cols * 2;
+  const int64_t row_off = row * sg.cols * 2;
   if (fmt == GNMR_FMT_BF16 && sg.in == sg.out) return;  // BF16 path in place: nothing to do
   const g_cvec* in = (const g_cvec*)(sg.in + row_off);
   g_vec* out = (g_vec*)(sg.out + row_off);
@@ -168,7 +170,8 @@ k4_actuate_wave(const RowItem* __restrict__ items, uint32_t num_rows,
   const uint32_t rows_per_wg = kK4Block / 64;
   const uint32_t r = xcd_order(blockIdx.x, gridDim.x) * rows_per_wg + (threadIdx.x >> 6);
   if (r >= num_rows) return;
-  actuate_row<64>(items[r], segs, mask, fmt_low, fmt_rec, int(threadIdx.x & 63), nullptr);
+  const RowItem it = items[r];
+  actuate_row<64>(segs[it.seg], it.row, mask, fmt_low, fmt_rec, int(threadIdx.x & 63), nullptr);
 }
 
 __global__ __launch_bounds__(kK4Block) __attribute__((amdgpu_waves_per_eu(6, 8))) void
@@ -176,7 +179,27 @@ k4_actuate(const RowItem* __restrict__ items, const ActSeg* __restrict__ segs,
            const uint8_t* __restrict__ mask, int fmt_low, int fmt_rec) {
   __shared__ float red[kK4Block / 64];
   const RowItem it = items[xcd_order(blockIdx.x, gridDim.x)];
-  actuate_row<kK4Block>(it, segs, mask, fmt_low, fmt_rec, int(threadIdx.x), red);
+  actuate_row<kK4Block>(segs[it.seg], it.row, mask, fmt_low, fmt_rec, int(threadIdx.x), red);
+}
+
+// One matrix without a row table (the segment passed by value): rows of at
+// most kK4WaveCols features, four per workgroup, one wavefront each.
+__global__ __launch_bounds__(kK4Block) __attribute__((amdgpu_waves_per_eu(6, 8))) void
+k4_matrix_wave(const ActSeg sg, int64_t num_rows, const uint8_t* __restrict__ mask, int fmt_low,
+               int fmt_rec) {
+  const int64_t r =
+      int64_t(xcd_order(blockIdx.x, gridDim.x)) * (kK4Block / 64) + (threadIdx.x >> 6);
+  if (r >= num_rows) return;
+  actuate_row<64>(sg, r, mask, fmt_low, fmt_rec, int(threadIdx.x & 63), nullptr);
+}
+
+// One matrix without a row table, rows longer than kK4WaveCols: one
+// workgroup per row.
+__global__ __launch_bounds__(kK4Block) __attribute__((amdgpu_waves_per_eu(6, 8))) void
+k4_matrix(const ActSeg sg, const uint8_t* __restrict__ mask, int fmt_low, int fmt_rec) {
+  __shared__ float red[kK4Block / 64];
+  actuate_row<kK4Block>(sg, xcd_order(blockIdx.x, gridDim.x), mask, fmt_low, fmt_rec,
+                        int(threadIdx.x), red);
 }
 
 }  // namespace
@@ -192,6 +215,20 @@ hipError_t launch_actuate(const RowItem* items, int64_t num_narrow, int64_t num_
   if (num_rows > num_narrow)
     hipLaunchKernelGGL(k4_actuate, dim3(unsigned(num_rows - num_narrow)), dim3(kK4Block), 0, s,
                        items + num_narrow, segs, mask, fmt_low, fmt_rec);
+  return hipGetLastError();
+}
+
+hipError_t launch_actuate_matrix(const ActSeg& sg, int64_t rows, const uint8_t* mask,
+                                 int fmt_low, int fmt_rec, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (sg.cols <= kK4WaveCols) {
+    const int64_t rows_per_wg = kK4Block / 64;
+    hipLaunchKernelGGL(k4_matrix_wave, dim3(unsigned((rows + rows_per_wg - 1) / rows_per_wg)),
+                       dim3(kK4Block), 0, s, sg, rows, mask, fmt_low, fmt_rec);
+  } else {
+    hipLaunchKernelGGL(k4_matrix, dim3(unsigned(rows)), dim3(kK4Block), 0, s, sg, mask, fmt_low,
+                       fmt_rec);
+  }
   return hipGetLastError();
 }
 

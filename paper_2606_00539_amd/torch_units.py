@@ -254,3 +254,84 @@ class FusedWgradUnits:
                 m.forward = f
         self._saved_forward = [None] * len(self.modules)
         self.ctl.close()
+
+
+_QUANT = None
+
+
+def _fake_quant_function():
+    """The autograd function of the actuator on a layer input: forward is the
+    per-token fake quantisation (gnmr_actuate_matrix), backward passes the
+    gradient straight through to the unquantised input."""
+    global _QUANT
+    if _QUANT is None:
+        import torch
+
+        from .binding import gnmr_actuate_matrix
+
+        class FakeQuantInput(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, x, d_mask, unit, fmt_low, fmt_recovery):
+                cols = x.shape[-1]
+                x2 = _kernel_operand(x, cols)
+                out = torch.empty_like(x2)
+                gnmr_actuate_matrix(x2, out, x2.shape[0], cols, d_mask, unit, fmt_low,
+                                    fmt_recovery, torch.cuda.current_stream())
+                return out.view(x.shape)
+
+            @staticmethod
+            def backward(ctx, g):
+                return g, None, None, None, None
+
+        _QUANT = FakeQuantInput
+    return _QUANT
+
+
+class QuantizedInputs:
+    """The recovery actuator inside a forward pass: each listed layer's input
+    is fake-quantised per token (K4, gnmr_actuate_matrix) before the layer
+    runs, in fmt_recovery when the layer's unit is in A_t and in fmt_low
+    otherwise (Alg. 2; App. E.2 quantisation-simulated operators; Sec. 5.1
+    token-wise low-bit activations), so the layer computes with, and saves for
+    its backward, the quantised activation.  The gradient reaches the
+    unquantised input unchanged (straight through).
+
+    `units` is a TorchUnits or FusedWgradUnits; a module is actuated when
+    its name (as given in `named_modules`) is one of units.unit_names, and
+    follows that unit's entry of the controller's device mask.  The mask is
+    read when each kernel runs, so the formats follow the latest controller
+    step in stream order, with no host synchronisation (before the first step
+    every unit is on the low-cost path).  Inputs must be bf16 with a last
+    dimension that is a multiple of 8 in [8, 16384].
+    """
+
+    def __init__(self, units, named_modules, fmt_low: int, fmt_recovery: int):
+        index = {n: b for b, n in enumerate(units.unit_names)}
+        self.units = units
+        self.d_mask = units.ctl.device_outputs()["mask"]
+        self.fmt_low, self.fmt_recovery = int(fmt_low), int(fmt_recovery)
+        self.handles, self.names = [], []
+        for name, m in named_modules:
+            if name not in index:
+                continue
+            self.handles.append(m.register_forward_pre_hook(self._hook(name, index[name])))
+            self.names.append(name)
+        if not self.handles:
+            raise ValueError("no module name matches a unit of the controller")
+
+    def _hook(self, name, unit):
+        import torch
+
+        fn = _fake_quant_function()
+
+        def hook(module, args):
+            x = args[0]
+            if x.dtype != torch.bfloat16 or not x.is_cuda:
+                raise TypeError(f"{name}: the input must be a bf16 tensor on a HIP device")
+            return (fn.apply(x, self.d_mask, unit, self.fmt_low, self.fmt_recovery),) + args[1:]
+        return hook
+
+    def close(self):
+        for h in self.handles:
+            h.remove()
+        self.handles = []

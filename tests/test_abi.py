@@ -152,6 +152,32 @@ def test_actuator_overlap_check_equals_brute_force():
     assert seen[True] > 50 and seen[False] > 50
 
 
+@pytest.mark.parametrize("bad", [
+    dict(cols=12), dict(cols=0), dict(cols=16392), dict(rows=-1), dict(rows=1 << 31),
+    dict(unit=-1), dict(fmt_low=6), dict(fmt_rec=-1), dict(x=4096 + 8), dict(out=8192 + 2),
+    dict(x=0), dict(mask=0), dict(out=4096 + 16), dict(x=8192 - 16),
+])
+def test_actuate_matrix_rejects_bad_arguments(bad):
+    # in [4096, 4608), out [8192, 8704): every case fails in the argument
+    # checks, before any device call
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    a = dict(x=4096, out=8192, rows=4, cols=64, mask=65536, unit=3, fmt_low=1, fmt_rec=0)
+    a.update(bad)
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_actuate_matrix(a["x"], a["out"], a["rows"], a["cols"], a["mask"], a["unit"],
+                              a["fmt_low"], a["fmt_rec"])
+    assert e.value.status == B.GNMR_E_INVALID
+
+
+def test_actuate_matrix_with_no_rows_launches_nothing():
+    # rows = 0 returns before any device call, whatever the pointers
+    from paper_2606_00539_amd import binding as B
+
+    B.gnmr_actuate_matrix(0, 0, 0, 64, 0, 0, 1, 0)
+
+
 def test_missing_library_fails_loudly(tmp_path):
     from paper_2606_00539_amd import binding as B
 

@@ -130,3 +130,88 @@ def test_actuator_segments_may_share_an_input():
     assert np.array_equal(outs[1].cpu().numpy().view(np.uint16).reshape(a.shape),
                           FQ.fakequant_rows(a, 5))
     assert np.array_equal(d_in.cpu().numpy().view(np.uint16).reshape(a.shape), a)
+
+
+MATRIX_CASES = [(5, 8), (37, 4096), (3, 4104), (2, 16384), (9, 1000), (0, 64), (1, 11008)]
+
+
+@pytest.mark.parametrize("rows,cols", MATRIX_CASES)
+@pytest.mark.parametrize("inplace", [False, True])
+def test_actuate_matrix_matches_oracle(rows, cols, inplace):
+    """The table-free entry: one matrix, both kernel shapes (a wavefront per
+    row up to 4096 features, a workgroup per longer row), the mask entry of
+    its unit choosing between two formats, bit-exact."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import gnmr_actuate_matrix
+
+    rng = np.random.default_rng(rows * 131 + cols + inplace)
+    x = rng.normal(size=(rows, cols)).astype(np.float32) * (10.0 ** rng.uniform(-4, 2, (rows, 1)))
+    if rows >= 3:
+        x[1] = 0.0
+        x[2, ::7] = -0.0
+    a = FQ.f32_to_bf16(x.astype(np.float32))
+    mask = torch.tensor([0, 1, 0], dtype=torch.uint8, device="cuda")
+    for unit, fmts in ((0, (3, 5)), (1, (2, 5)), (2, (0, 1))):
+        d_in = to_device(torch, a)
+        d_out = d_in if inplace else torch.full_like(d_in, 0x5555)
+        gnmr_actuate_matrix(d_in, d_out, rows, cols, mask, unit, *fmts)
+        torch.cuda.synchronize()
+        want = FQ.fakequant_rows(a, fmts[1] if unit == 1 else fmts[0])
+        got = d_out.cpu().numpy().view(np.uint16).reshape(a.shape)
+        assert np.array_equal(got, want), f"unit {unit} fmts {fmts}"
+        if not inplace:
+            assert np.array_equal(d_in.cpu().numpy().view(np.uint16).reshape(a.shape), a)
+
+
+def test_quantized_inputs_follow_the_controller():
+    """QuantizedInputs on three bf16 linear layers registered as units: before
+    any step every layer takes the low-cost format; after a step that puts
+    layer 1 in A_t, layer 1 takes the recovery format.  Outputs equal the
+    layer applied to the oracle's quantised input, bit for bit; the input
+    gradient is the straight-through one."""
+    torch = require_gpu()
+    import torch.nn.functional as F
+
+    from paper_2606_00539_amd import GNMR_FMT_E2M1, GNMR_FMT_INT8
+    from paper_2606_00539_amd.torch_units import QuantizedInputs, TorchUnits
+
+    torch.manual_seed(0)
+    layers = torch.nn.ModuleDict({f"l{i}": torch.nn.Linear(256, 64 * (i + 1), bias=i == 2)
+                                  for i in range(3)}).to("cuda", torch.bfloat16)
+    units = TorchUnits([(n + ".weight", m.weight) for n, m in layers.items()],
+                       window=5, max_o=1, lock_len=1, eps=0.0,
+                       unit_of=lambda name: name[:-len(".weight")])
+    quant = QuantizedInputs(units, layers.items(), GNMR_FMT_E2M1, GNMR_FMT_INT8)
+
+    def check(expect_fmt):
+        for b, (n, m) in enumerate(layers.items()):
+            x = (torch.randn(2, 9, 256, device="cuda") * (b + 1)).to(torch.bfloat16)
+            x.requires_grad_(True)
+            y = m(x)
+            xb = x.detach().cpu().view(torch.int16).numpy().view(np.uint16).reshape(-1, 256)
+            xq = torch.from_numpy(FQ.fakequant_rows(xb, expect_fmt[b]).view(np.int16)).to("cuda")
+            xq = xq.view(torch.bfloat16).reshape(x.shape).requires_grad_(True)
+            ref = F.linear(xq, m.weight, m.bias)
+            assert torch.equal(y, ref), f"{n}: output differs"
+            dy = torch.randn_like(y)
+            y.backward(dy)
+            ref.backward(dy)
+            assert torch.equal(x.grad, xq.grad), f"{n}: input gradient is not straight through"
+
+    try:
+        check([GNMR_FMT_E2M1] * 3)
+        norms = torch.ones(3, dtype=torch.float64, device="cuda")
+        for _ in range(6):
+            units.ctl.step_from_norms(norms, 1.1, 1.5)
+        norms[1] = 9.0                                  # layer 1 spikes -> A_t = {1}
+        units.ctl.step_from_norms(norms, 1.1, 1.5)
+        assert units.query()["mask"].tolist() == [0, 1, 0]
+        check([GNMR_FMT_E2M1, GNMR_FMT_INT8, GNMR_FMT_E2M1])
+        with pytest.raises(TypeError):
+            layers["l0"](torch.randn(4, 256, device="cuda"))     # fp32 input
+    finally:
+        quant.close()
+        units.close()
+    # hooks removed: the layer sees its input unchanged
+    x = torch.randn(3, 256, device="cuda").to(torch.bfloat16)
+    assert torch.equal(layers["l0"](x), F.linear(x, layers["l0"].weight))
