@@ -3,7 +3,7 @@ controller's mask) against its oracle, bit for bit, through the C ABI."""
 import numpy as np
 import pytest
 
-from gpu_util import require_gpu
+from gpu_util import assert_step_matches, require_gpu
 from oracle import fakequant as FQ
 
 pytestmark = pytest.mark.gpu
@@ -215,3 +215,85 @@ def test_quantized_inputs_follow_the_controller():
     # hooks removed: the layer sees its input unchanged
     x = torch.randn(3, 256, device="cuda").to(torch.bfloat16)
     assert torch.equal(layers["l0"](x), F.linear(x, layers["l0"].weight))
+
+
+def test_training_loop_with_controller_and_actuator():
+    """A few SGD steps of a small SwiGLU stack in bf16 with the whole loop in
+    place: each projection's input quantised per token by QuantizedInputs
+    (E2M1 on the low-cost path, BF16 on the recovery path) from the mask of
+    the previous controller step, the controller stepping over the .grad
+    buffers (reallocated every step by zero_grad(set_to_none=True)), and the
+    optimizer.  Every layer input the hooks produced is the oracle's
+    quantisation of the layer's real input under that mask; every controller
+    step matches the oracle fed with float64 norms of the stored gradients."""
+    torch = require_gpu()
+    import torch.nn.functional as F
+
+    from oracle import Controller as Oracle
+    from oracle import unit_norm
+    from paper_2606_00539_amd import GNMR_FMT_BF16, GNMR_FMT_E2M1
+    from paper_2606_00539_amd.torch_units import QuantizedInputs, TorchUnits, llama_linear_units
+
+    torch.manual_seed(3)
+    d, f = 64, 128
+    model = torch.nn.ModuleDict({"layers": torch.nn.ModuleList([
+        torch.nn.ModuleDict({"gate_proj": torch.nn.Linear(d, f, bias=False),
+                             "up_proj": torch.nn.Linear(d, f, bias=False),
+                             "down_proj": torch.nn.Linear(f, d, bias=False)})
+        for _ in range(2)])}).to("cuda", torch.bfloat16)
+    params = list(model.named_parameters())
+    units = TorchUnits(params, max_o=2, lock_len=1, eps=1e-12, unit_of=llama_linear_units)
+    U = len(units.unit_names)
+    assert U == 6
+    ora = Oracle(U, window=5, max_o=2, lock_len=1, eps=1e-12)
+    seen = {}
+
+    def capture(name):
+        def pre(module, args):
+            seen[name] = [args[0].detach().clone()]
+        return pre
+
+    def after(name):
+        def post(module, args, out):
+            seen[name].append(args[0].detach().clone())
+        return post
+
+    named = [(n, m) for n, m in model.named_modules() if n in units.unit_names]
+    hooks = [m.register_forward_pre_hook(capture(n)) for n, m in named]
+    quant = QuantizedInputs(units, named, GNMR_FMT_E2M1, GNMR_FMT_BF16)
+    hooks += [m.register_forward_hook(after(n)) for n, m in named]
+    opt = torch.optim.SGD(model.parameters(), lr=0.5)
+
+    def bits(t):
+        return t.view(torch.int16).cpu().numpy().view(np.uint16).reshape(-1, t.shape[-1])
+
+    mask_prev = np.zeros(U, np.uint8)
+    recovered = 0
+    try:
+        for t in range(1, 9):
+            x = torch.randn(2, 16, d, device="cuda").to(torch.bfloat16)
+            h = x
+            for blk in model["layers"]:
+                h = h + blk["down_proj"](F.silu(blk["gate_proj"](h)) * blk["up_proj"](h))
+            loss = (h.float() ** 2).mean()
+            loss.backward()
+            for b, u in enumerate(units.unit_names):
+                orig, used = seen[u]
+                fmt = GNMR_FMT_BF16 if mask_prev[b] else GNMR_FMT_E2M1
+                assert np.array_equal(bits(used), FQ.fakequant_rows(bits(orig), fmt)), \
+                    f"t={t} {u}: the layer did not see its input in format {fmt}"
+            units.step(0.9, 1.5)                      # alpha < 1: every unit is a candidate
+            out = units.query()
+            norms = [unit_norm([(bits(p.grad).ravel(), 1)]) for p in units.params]
+            assert_step_matches(out, ora.step(norms, 0.9, 1.5), rtol=1e-5, what=f"t={t}")
+            assert out["mask"].sum() <= 2
+            recovered += int(out["mask"].sum())
+            mask_prev = out["mask"].copy()
+            opt.step()
+            opt.zero_grad(set_to_none=True)
+        assert recovered > 0
+    finally:
+        for hk in hooks:
+            hk.remove()
+        quant.close()
+        units.close()
