@@ -34,5 +34,34 @@ def build(verbose: bool = True) -> str:
     return LIB
 
 
+# AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (the
+# device code is built as usual); any undefined behaviour aborts.
+HOST_SANITIZE_FLAGS = ["-O1", "-g", "-shared-libsan",
+                       "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                       "-Xarch_host", "-fno-sanitize-recover=undefined",
+                       "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def sanitizer_runtime():
+    """The clang AddressSanitizer runtime that a process loading the
+    host-sanitized library must preload, or None if this toolchain has none."""
+    import glob
+
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    found = sorted(glob.glob(os.path.join(rocm, "llvm", "lib", "clang", "*", "lib", "linux",
+                                          "libclang_rt.asan-x86_64.so")))
+    return found[-1] if found else None
+
+
+def build_host_sanitized(out_path: str) -> str:
+    """libgnmr.so with the host code under the sanitizers, at out_path (for
+    CPU tests of the host logic: argument checks, work lists, overlap checks,
+    error paths)."""
+    cmd = [hipcc(), *HIPCC_FLAGS, *HOST_SANITIZE_FLAGS, "-I", os.path.join(ROOT, "include"),
+           "-o", out_path, *SOURCES]
+    subprocess.run(cmd, check=True, stdout=subprocess.DEVNULL, stderr=subprocess.PIPE)
+    return out_path
+
+
 if __name__ == "__main__":
     build(verbose="-q" not in sys.argv)

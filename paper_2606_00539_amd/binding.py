@@ -13,7 +13,9 @@ import os
 
 import numpy as np
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgnmr.so")
+# GNMR_LIBRARY names another build of the same library (e.g. a host-sanitizer one)
+_LIB_PATH = os.environ.get("GNMR_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libgnmr.so")
 
 GNMR_OK, GNMR_E_INVALID, GNMR_E_NOMEM, GNMR_E_HIP, GNMR_E_STATE = 0, -1, -2, -3, -4
 GNMR_F32, GNMR_BF16 = 0, 1
