@@ -294,7 +294,9 @@ typedef struct gnmr_actuator gnmr_actuator;
 
 /* Build the row work list over the segments (host array, copied; the caller
  * may free it).  num_units bounds the unit indices.  Allocates device memory
- * for the tables (8 B per row, 24 B per segment). */
+ * for the tables (8 B per row, 24 B per segment).  At most 67,108,860 rows of
+ * up to 4096 features and 16,777,215 longer rows in all (the most one
+ * launch's grid can hold); GNMR_E_INVALID beyond. */
 gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* segs,
                                  int64_t num_segments, int32_t num_units, void* stream);
 
@@ -310,7 +312,8 @@ gnmr_status gnmr_actuate(gnmr_actuator* act, const uint8_t* d_mask, int32_t fmt_
  * buffers change every call, such as the input of one linear layer inside a
  * forward pass.  in: device bf16 [rows][cols], row-major, 16-byte aligned;
  * out: equal to `in` (in place) or not overlapping it, 16-byte aligned; cols
- * a multiple of 8 in [8, 16384]; 0 <= rows < 2^31; the matrix takes
+ * a multiple of 8 in [8, 16384]; 0 <= rows <= 67,108,860 (cols <= 4096) or
+ * 16,777,215 (longer rows), the most one launch's grid can hold; the matrix takes
  * fmt_recovery when d_mask[unit] != 0, else fmt_low (d_mask: device bytes,
  * e.g. the controller's mask from gnmr_device_outputs, read when the kernel
  * runs).  Allocates nothing and launches one kernel (none when rows = 0);

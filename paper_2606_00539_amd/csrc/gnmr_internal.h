@@ -81,6 +81,10 @@ constexpr int kK4Block = 256;
 constexpr int kK4Vpt = 8;
 constexpr int kK4WaveCols = 64 * kK4Vpt * 8;
 constexpr int kK4MaxCols = kK4Block * kK4Vpt * 8;
+// A launch's grid holds fewer than 2^32 work items: at most this many
+// workgroups of kK4Block lanes, i.e. this many wide rows or four times as many
+// narrow ones per launch.
+constexpr int64_t kK4MaxWorkgroups = int64_t(UINT32_MAX) / kK4Block;
 
 struct ActSeg {
   const char* in;

@@ -597,6 +597,8 @@ int64_t gnmr_wgrad_num_tiles(int32_t out_features, int32_t in_features) {
   return gnmr::wgrad_tiles(out_features, in_features);
 }
 
+constexpr int64_t kWgMaxTiles = int64_t(UINT32_MAX) / gnmr::kWgThreads;
+
 gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t num_problems,
                                      float* tile_sumsq, void* stream) {
   if (num_problems < 0 || (num_problems > 0 && problems == nullptr))
@@ -617,8 +619,9 @@ gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t
     if ((reinterpret_cast<uintptr_t>(q.dy) | reinterpret_cast<uintptr_t>(q.x) |
          reinterpret_cast<uintptr_t>(q.dw)) % 16 != 0)
       return fail(GNMR_E_INVALID, "dy, x and dw must be 16-byte aligned");
-    if (gnmr::wgrad_tiles(q.out_features, q.in_features) > int64_t(INT32_MAX / 2))
-      return fail(GNMR_E_INVALID, "too many output tiles");
+    // one workgroup of kWgThreads lanes per tile; a grid holds < 2^32 lanes
+    if (gnmr::wgrad_tiles(q.out_features, q.in_features) > kWgMaxTiles)
+      return fail(GNMR_E_INVALID, "too many output tiles for one launch");
     if (q.accumulate != 0 && q.accumulate != 1)
       return fail(GNMR_E_INVALID, "accumulate must be 0 or 1");
     if (q.reserved != 0) return fail(GNMR_E_INVALID, "reserved must be 0");
@@ -654,7 +657,7 @@ gnmr_status gnmr_wgrad_sumsq_batched(const gnmr_wgrad_problem* problems, int32_t
     while (i < num_problems && b.num < gnmr::kWgMaxBatch) {
       const gnmr_wgrad_problem& q = problems[i];
       const int64_t t = gnmr::wgrad_tiles(q.out_features, q.in_features);
-      if (b.num > 0 && tiles + t > int64_t(INT32_MAX / 2)) break;
+      if (b.num > 0 && tiles + t > kWgMaxTiles) break;
       gnmr::WgProblem& P = b.p[b.num++];
       P.dy = static_cast<const uint16_t*>(q.dy);
       P.x = static_cast<const uint16_t*>(q.x);
@@ -894,6 +897,16 @@ gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* se
     bytes += g.rows * int64_t(g.cols) * 2;
   }
   if (rows > int64_t(UINT32_MAX)) return fail(GNMR_E_INVALID, "too many rows in total");
+  {
+    int64_t narrow_rows = 0;
+    for (int64_t k = 0; k < num_segments; ++k)
+      if (segs[k].cols <= gnmr::kK4WaveCols) narrow_rows += segs[k].rows;
+    if (narrow_rows > 4 * gnmr::kK4MaxWorkgroups || rows - narrow_rows > gnmr::kK4MaxWorkgroups)
+      return fail(GNMR_E_INVALID, "too many rows for one launch: at most " +
+                                      std::to_string(4 * gnmr::kK4MaxWorkgroups) +
+                                      " rows of up to 4096 features and " +
+                                      std::to_string(gnmr::kK4MaxWorkgroups) + " longer rows");
+  }
   // A segment writes in place or into memory that no segment reads, and no
   // two segments write the same bytes.
   {
@@ -981,6 +994,11 @@ gnmr_status gnmr_actuate_matrix(const void* in, void* out, int64_t rows, int32_t
   if (rows < 0 || rows > INT32_MAX) return fail(GNMR_E_INVALID, "rows must be in [0, 2^31)");
   if (cols < 8 || cols > gnmr::kK4MaxCols || cols % 8 != 0)
     return fail(GNMR_E_INVALID, "cols must be a multiple of 8 in [8, 16384]");
+  if (rows > (cols <= gnmr::kK4WaveCols ? 4 : 1) * gnmr::kK4MaxWorkgroups)
+    return fail(GNMR_E_INVALID, "too many rows for one launch: at most " +
+                                    std::to_string(4 * gnmr::kK4MaxWorkgroups) +
+                                    " rows of up to 4096 features or " +
+                                    std::to_string(gnmr::kK4MaxWorkgroups) + " longer rows");
   if (unit < 0) return fail(GNMR_E_INVALID, "unit must be >= 0");
   if (fmt_low < GNMR_FMT_BF16 || fmt_low > GNMR_FMT_INT8 || fmt_recovery < GNMR_FMT_BF16 ||
       fmt_recovery > GNMR_FMT_INT8)

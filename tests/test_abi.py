@@ -123,6 +123,21 @@ def _races(segs):
     return False
 
 
+@pytest.mark.parametrize("segs", [
+    [(1 << 40, 2 << 40, 4 * 16777215 + 1, 8, 0)],
+    [(1 << 40, 2 << 40, 3 * 16777215, 8, 0), (3 << 40, 4 << 40, 16777216, 8, 1)],
+    [(1 << 40, 2 << 40, 16777216, 4104, 0)],
+])
+def test_actuator_rejects_more_rows_than_one_launch_holds(segs):
+    # the limit is checked before any allocation or device call
+    from paper_2606_00539_amd import GnmrError
+    from paper_2606_00539_amd import binding as B
+
+    with pytest.raises(GnmrError) as e:
+        B.gnmr_actuator_create(segs, num_units=2)
+    assert e.value.status == B.GNMR_E_INVALID and "one launch" in B.gnmr_last_error()
+
+
 def test_actuator_overlap_check_equals_brute_force():
     # random layouts of fake addresses; a layout without a race passes the
     # checks and fails only later, at the table allocation (no device here),
@@ -155,6 +170,7 @@ def test_actuator_overlap_check_equals_brute_force():
 @pytest.mark.parametrize("bad", [
     dict(cols=12), dict(cols=0), dict(cols=16392), dict(rows=-1), dict(rows=1 << 31),
     dict(unit=-1), dict(fmt_low=6), dict(fmt_rec=-1), dict(x=4096 + 8), dict(out=8192 + 2),
+    dict(rows=4 * 16777215 + 1, cols=8), dict(rows=16777216, cols=4104),
     dict(x=0), dict(mask=0), dict(out=4096 + 16), dict(x=8192 - 16),
 ])
 def test_actuate_matrix_rejects_bad_arguments(bad):
@@ -197,7 +213,7 @@ def test_bench_refuses_more_than_one_gpu():
 @pytest.mark.parametrize("bad", [
     dict(out_f=12), dict(in_f=4), dict(out_f=0), dict(in_f=-8), dict(tokens=-1),
     dict(dy=0), dict(x=0), dict(dw=0), dict(ss=0), dict(dy=4096 + 8), dict(dw=8192 + 2),
-    dict(in_f=1 << 24), dict(out_f=1 << 24),
+    dict(in_f=1 << 24), dict(out_f=1 << 24), dict(out_f=1 << 20, in_f=1 << 20),
 ])
 def test_wgrad_rejects_bad_arguments(bad):
     # every case fails in the argument checks, before any device call
