@@ -113,8 +113,10 @@ typedef struct {
 /* Create a controller: t = 0, A = 0, Q empty, Lock = 0 (the state before the
  * first step of Alg. 1 / Alg. 2).  Allocates all device state (O(U * delta)
  * doubles plus one float per 64 KiB work item) and builds the work list over
- * the segments.  `stream` orders the initial clears.  *out receives the
- * context, or NULL on error. */
+ * the segments: each segment takes one item per started 64 KiB, at most
+ * 16,777,215 items in all (the most one launch's grid can hold), and
+ * seg_numel <= 2^50; GNMR_E_INVALID beyond.  `stream` orders the initial
+ * clears.  *out receives the context, or NULL on error. */
 gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg,
                       const gnmr_segments* segs, void* stream);
 

@@ -348,10 +348,21 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   for (int64_t b = 0; b < U; ++b)
     if (segs->unit_seg_off[b + 1] < segs->unit_seg_off[b])
       return fail(GNMR_E_INVALID, "unit_seg_off must be non-decreasing");
+  // one K1 workgroup per item, and a grid holds fewer than 2^32 lanes
+  const int64_t max_items = int64_t(UINT32_MAX) / gnmr::kK1Block;
+  int64_t num_items = 0;
   for (int64_t s = 0; s < S; ++s) {
-    if (segs->seg_numel[s] < 0) return fail(GNMR_E_INVALID, "negative seg_numel");
+    const int64_t n = segs->seg_numel[s];
+    if (n < 0) return fail(GNMR_E_INVALID, "negative seg_numel");
     if (segs->seg_dtype[s] != GNMR_F32 && segs->seg_dtype[s] != GNMR_BF16)
       return fail(GNMR_E_INVALID, "unknown seg_dtype " + std::to_string(segs->seg_dtype[s]));
+    const int64_t per = gnmr::kItemBytes / (segs->seg_dtype[s] == GNMR_BF16 ? 2 : 4);
+    if (n > (int64_t(1) << 50)) return fail(GNMR_E_INVALID, "seg_numel above 2^50");
+    num_items += (n + per - 1) / per;  // at most 2^37 more: no overflow before the test
+    if (num_items > max_items)
+      return fail(GNMR_E_INVALID, "too many work items for one launch: more than " +
+                                      std::to_string(max_items) +
+                                      " (each segment takes one item per started 64 KiB)");
   }
 
   gnmr_ctx* c = new (std::nothrow) gnmr_ctx;
@@ -388,10 +399,6 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
     unit_item_off[size_t(b) + 1] = int64_t(items.size());
   }
   c->num_items = int64_t(items.size());
-  if (c->num_items > int64_t(UINT32_MAX)) {
-    delete c;
-    return fail(GNMR_E_INVALID, "too many work items");
-  }
 
   // One device arena for all state.
   const size_t a = 256;

@@ -46,7 +46,10 @@ def test_struct_layouts_match_header():
 @pytest.mark.parametrize("bad", [
     dict(num_units=0), dict(window=0), dict(max_o=-1), dict(lock_len=-2), dict(eps=-1.0),
     dict(eps=float("nan")), dict(unit_seg_off=[0, 2, 1]), dict(unit_seg_off=[1, 1, 1]),
-    dict(seg_numel=[-1]), dict(seg_dtype=[7]), dict(budget_mode=3), dict(warmup_steps=-1), dict(budget_mode=2, warmup_steps=0),
+    dict(seg_numel=[-1]), dict(seg_dtype=[7]), dict(budget_mode=3), dict(warmup_steps=-1),
+    dict(budget_mode=2, warmup_steps=0),
+    dict(seg_numel=[(1 << 50) + 1]),                     # above 2^50 elements
+    dict(seg_numel=[16777215 * 32768 + 1]),              # one bf16 item too many
 ])
 def test_init_rejects_bad_configuration(bad):
     from paper_2606_00539_amd import GnmrError, gnmr_init
