@@ -297,3 +297,63 @@ def test_training_loop_with_controller_and_actuator():
             hk.remove()
         quant.close()
         units.close()
+
+
+def test_actuator_fullsize_bench_configuration():
+    """The benchmark's launch configuration: one actuator over the saved
+    activations of the 7 projections of 32 LLaMA-2-7B layers at 4,096 tokens
+    (224 units, 9.33 GB, in place), 8 units on the recovery path (BF16), the
+    rest on E2M1.  Sampled rows of every unit kind are checked bit for bit
+    against the oracle; every row is checked against properties that hold at
+    any size (recovery rows untouched, signs kept, magnitudes within the row's
+    largest one, the largest one kept)."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import GNMR_FMT_BF16, GNMR_FMT_E2M1, Actuator
+
+    tokens, U = 4096, 32 * 7
+    cols = [4096] * 6 + [11008]
+    shapes = [(tokens, cols[b % 7]) for b in range(U)]
+    total = sum(r * c for r, c in shapes)
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    buf = torch.randn(total, dtype=torch.float32, device="cuda", generator=gen).to(torch.bfloat16)
+    segs, offs, off = [], [], 0
+    for b, (r, c) in enumerate(shapes):
+        p = buf.data_ptr() + 2 * off
+        segs.append((p, p, r, c, b))
+        offs.append(off)
+        off += r * c
+    mask = np.zeros(U, np.uint8)
+    rec = np.random.default_rng(0).choice(U, 8, replace=False)
+    mask[rec] = 1
+    rng = np.random.default_rng(1)
+    picks = [(b, int(r)) for b in sorted(set(rng.choice(U, 24, replace=False)) | set(rec[:2]) |
+                                         {0, U - 1})
+             for r in (0, tokens - 1, *rng.choice(tokens, 2, replace=False))]
+
+    def row(t, b, r):
+        c = shapes[b][1]
+        return t[offs[b] + r * c: offs[b] + (r + 1) * c]
+
+    before = {(b, r): row(buf, b, r).view(torch.int16).cpu().numpy().view(np.uint16)
+              for b, r in picks}
+    orig = buf.clone()
+    with Actuator(segs, U) as act:
+        act.apply(torch.from_numpy(mask).to("cuda"), GNMR_FMT_E2M1, GNMR_FMT_BF16)
+        torch.cuda.synchronize()
+    for b, r in picks:
+        got = row(buf, b, r).view(torch.int16).cpu().numpy().view(np.uint16)
+        fmt = GNMR_FMT_BF16 if mask[b] else GNMR_FMT_E2M1
+        want = FQ.fakequant_rows(before[(b, r)][None, :], fmt)[0]
+        assert np.array_equal(got, want), f"unit {b} row {r}"
+    for b, (r, c) in enumerate(shapes):
+        x = orig[offs[b]:offs[b] + r * c].view(r, c).float()
+        y = buf[offs[b]:offs[b] + r * c].view(r, c).float()
+        if mask[b]:
+            assert torch.equal(x, y), f"unit {b}: a recovery-path row changed"
+            continue
+        amax = x.abs().amax(dim=1, keepdim=True)
+        assert bool(((y == 0) | (torch.sign(y) == torch.sign(x))).all()), f"unit {b}: sign"
+        assert bool((y.abs() <= amax * (1 + 2.0 ** -7)).all()), f"unit {b}: magnitude"
+        ymax = y.abs().amax(dim=1, keepdim=True)
+        assert bool(((ymax - amax).abs() <= amax * 2.0 ** -7).all()), f"unit {b}: row maximum"
+    del orig, buf
