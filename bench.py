@@ -364,6 +364,15 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     ms_unfused = timed(unfused_step, steps)
     ms_k5 = timed(lambda _: gemms_only("k5"), steps)
     ms_blas = timed(lambda _: gemms_only("blas"), steps)
+    # gradient accumulation over micro-batches: dw += dy^T x (K5's accumulate
+    # flag; the library's beta = 1 product); the stored gradient is read too
+    acc_problems = [p + (1,) for p in problems]
+    ms_k5_acc = timed(lambda _: gnmr_wgrad_sumsq_batched(acc_problems, parts, stream), steps)
+
+    def blas_acc(_):
+        for b in range(U):
+            dws[b].addmm_(dys[b].t(), xs[b])
+    ms_blas_acc = timed(blas_acc, steps)
     # per-shape K5 and library GEMM times (the dominant kernel's roofline)
     per_shape = {}
     for b, (o, i) in enumerate(L.shapes[:1] + L.shapes[4:5] + L.shapes[6:7]):
@@ -399,6 +408,10 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
                     "hipblaslt_gemms_ms": round(ms_blas, 4),
                     "gnmr_step_ms": round(ms_unfused - ms_blas, 4)},
         "fused_saving_ms": round(ms_unfused - ms_fused, 4),
+        "accumulate": {"k5_ms": round(ms_k5_acc, 4),
+                       "k5_tflops": round(L.flops / (ms_k5_acc * 1e-3) / 1e12, 1),
+                       "hipblaslt_ms": round(ms_blas_acc, 4),
+                       "hipblaslt_tflops": round(L.flops / (ms_blas_acc * 1e-3) / 1e12, 1)},
         "per_shape": per_shape}), flush=True)
     fused.close()
     unfused.close()
