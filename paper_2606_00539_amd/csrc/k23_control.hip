@@ -413,9 +413,18 @@ __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) { select_bod
 // K2 and K3 in one workgroup, for small workloads: at most kK3Block units,
 // each summed by one thread exactly as k2_update<1> sums it (or given its
 // norm), then the selection of K3 after a workgroup barrier, which makes
-// K2's keys, flags, candidate list and counters visible to every thread.
-// One launch instead of two; the same arithmetic, so the same results.
+// K2's keys and flags visible to every thread.  The counters and the
+// candidate list live in LDS here (one workgroup uses them), which keeps
+// global atomics off the path.  One launch instead of two; the same
+// arithmetic, so the same results.
 __global__ __launch_bounds__(kK3Block) void k23_small(UpdateArgs u, SelectArgs s) {
+  __shared__ int32_t s_counters[kNumCounters];
+  __shared__ int32_t s_cand[kK3Block];
+  if (threadIdx.x < kNumCounters) s_counters[threadIdx.x] = 0;
+  u.counters = s.counters = s_counters;
+  u.cand_list = s_cand;
+  s.cand_list = s_cand;
+  __syncthreads();
   const int b = int(threadIdx.x);
   if (b < u.num_units) {
     const double n = u.ext_norm != nullptr
