@@ -232,15 +232,31 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
       if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (tid == 0) {
-      uint32_t cum = 0;
-      int d = 255;
-      for (; d > 0; --d) {
-        if (cum + hist[d] >= uint32_t(k)) break;
-        cum += hist[d];
+    if (tid < 64) {
+      // The digit of the k-th largest key: the largest d whose count of keys
+      // with a digit above d is below k, found by one wavefront: lane l holds
+      // digits 4l .. 4l+3, a suffix sum over the lanes gives the count above
+      // each lane's digits, and the one lane whose digits reach k names d
+      // (k <= the keys in the histogram, so exactly one lane does).
+      const int l = tid;
+      const uint32_t h0 = hist[4 * l], h1 = hist[4 * l + 1], h2 = hist[4 * l + 2],
+                     h3 = hist[4 * l + 3];
+      const uint32_t own = h0 + h1 + h2 + h3;
+      uint32_t suffix = own;  // keys with a digit >= 4l
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t v = __shfl_down(suffix, off, 64);
+        if (l + off < 64) suffix += v;
       }
-      *s_digit = d;
-      *s_k = k - int(cum);
+      uint32_t above = suffix - own;  // keys with a digit above 4l+3
+      const uint32_t uk = uint32_t(k);
+      if (above < uk && above + own >= uk) {
+        int d = 4 * l + 3;
+        const uint32_t h[4] = {h0, h1, h2, h3};
+        for (int j = 3; j > 0 && above + h[j] < uk; --j, --d) above += h[j];
+        *s_digit = d;
+        *s_k = k - int(above);
+      }
     }
     __syncthreads();
     prefix |= uint64_t(*s_digit) << shift;
@@ -311,11 +327,12 @@ __device__ void bitonic_sort(int32_t* v) {
 // K3: a single workgroup, over the members of C_t listed by K2.  Kept units
 // (warm-up; continuing units under the admitted-only budget) are active
 // without ranking; the others are ranked for the budget.  When at most maxO
-// are ranked they are all active.  Otherwise Top_maxO needs the maxO-th
-// largest ranked key T (radix select; kept units carry key 0): every ranked
-// candidate with key > T is active, and the first `need` with key == T in
-// index order.  Pools of up to kK3Cap candidates are ranked in LDS; larger
-// ones over the global keys of all units.
+// are ranked they are all active.  Otherwise pools of at most one candidate
+// per thread count each candidate's place in the order directly; larger
+// ones need the maxO-th largest ranked key T (radix select; kept units carry
+// key 0): every ranked candidate with key > T is active, and the first
+// `need` with key == T in index order.  Pools of up to kK3Cap candidates are
+// ranked in LDS; larger ones over the global keys of all units.
 __device__ void select_body(const SelectArgs& a) {
   __shared__ uint64_t c_key[kK3Cap];
   __shared__ int32_t c_idx[kK3Cap];
@@ -339,6 +356,32 @@ __device__ void select_body(const SelectArgs& a) {
       const int b = a.cand_list[i];
       const uint8_t f = a.flags[b];
       const bool sel = take || (f & kFlagKeep);
+      apply_selection(a, b, sel, f);
+      c_act += sel;
+    }
+  } else if (n_cand <= kK3Block) {
+    // A pool of at most one candidate per thread: each ranked candidate's
+    // place in the order (R descending, index ascending) is counted
+    // directly against the whole pool, one barrier instead of the radix
+    // passes.  Kept units carry key 0, below every ranked key, so they never
+    // push a ranked one down; a ranked candidate is active when fewer than
+    // maxO candidates come before it.
+    if (tid < n_cand) {
+      const int b = a.cand_list[tid];
+      c_idx[tid] = b;
+      c_key[tid] = a.keys[b];
+    }
+    __syncthreads();
+    if (tid < n_cand) {
+      const int b = c_idx[tid];
+      const uint64_t key = c_key[tid];
+      int before = 0;
+      for (int j = 0; j < n_cand && before < a.max_o; ++j) {
+        const uint64_t kj = c_key[j];
+        before += (kj > key || (kj == key && c_idx[j] < b)) ? 1 : 0;
+      }
+      const uint8_t f = a.flags[b];
+      const bool sel = (key != 0 && before < a.max_o) || (f & kFlagKeep);
       apply_selection(a, b, sel, f);
       c_act += sel;
     }

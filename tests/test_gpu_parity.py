@@ -285,12 +285,15 @@ def test_abi_errors_leave_state_unchanged():
         assert ctl.query()["stats"]["t"] == 2
 
 
-@pytest.mark.parametrize("case", ["few_ties_at_cut", "many_ties_at_cut", "huge_pool",
-                                  "pool_at_capacity"])
+@pytest.mark.parametrize("case", ["few_ties_at_cut", "mid_pool_ties_at_cut", "many_ties_at_cut",
+                                  "huge_pool", "pool_at_capacity", "pool_of_one_per_thread"])
 def test_selection_paths(case):
-    """Top_maxO through each selection path of the kernel: candidates ranked in
-    LDS with index-ordered ties at the cut, more ties than the tie buffer,
-    more candidates than the LDS pool (global keys), and a pool right at it."""
+    """Top_maxO through each selection path of the kernel: a pool of at most
+    one candidate per thread ranked by direct counting, with index-ordered
+    ties at the cut (few_ties_at_cut) and at exactly 1,024 candidates; larger
+    pools by radix select in LDS with the ties at the cut sorted
+    (mid_pool_ties_at_cut), more ties than the tie buffer, more candidates
+    than the LDS pool (global keys), and a pool right at it."""
     torch = require_gpu()
     from paper_2606_00539_amd import Controller
 
@@ -304,6 +307,19 @@ def test_selection_paths(case):
         base[9, tied] *= 6.0
         base[9, tied[:20]] *= 3.0
         base[9, tied[:20]] += np.arange(20)       # distinct keys above the tie
+    elif case == "mid_pool_ties_at_cut":
+        # about 2,000 candidates: 20 distinct spikes, a 300-unit tie holding
+        # the cut, and 1,700 weaker spikes below it
+        perm = rng.permutation(U)
+        tied, strong, weak = perm[:300], perm[300:320], perm[320:2020]
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+        base[9, strong] *= 18.0 + np.arange(20)
+        base[9, weak] *= 2.0
+    elif case == "pool_of_one_per_thread":
+        U = 3000
+        base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
+        base[9, :1024] *= 6.0 + rng.random(1024)   # exactly 1,024 candidates at t = 10
     elif case == "many_ties_at_cut":
         tied = rng.choice(U, 1500, replace=False)
         base[:, tied] = base[:, tied[:1]]
@@ -327,6 +343,10 @@ def test_selection_paths(case):
             assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} t={t}")
             if case == "pool_at_capacity" and t == 10:
                 assert ref.stats["n_cand"] == 4096
+            if case == "pool_of_one_per_thread" and t == 10:
+                assert ref.stats["n_cand"] == 1024
+            if case == "mid_pool_ties_at_cut" and t == 10:
+                assert 1024 < ref.stats["n_cand"] <= 4096
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama2-13b", "moe", "fine32"])
