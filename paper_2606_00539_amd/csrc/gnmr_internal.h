@@ -20,6 +20,14 @@ enum : int {
   kNumCounters = 8
 };
 
+// K2 spreads its counters and candidate list over this many sets (workgroup
+// w adds to set w % kCounterSets), so that its global atomics do not queue
+// on one address; K3 gathers the sets.
+constexpr int kCounterSets = 64;
+// Entries per set of the candidate list for U units: a set receives at most
+// ceil(workgroups / kCounterSets) workgroups of at most 256 units each.
+inline int64_t cand_list_cap(int64_t num_units) { return num_units / kCounterSets + 512; }
+
 // Per-unit flag bits written by K2 and read by K3.
 enum : uint8_t {
   kFlagTrigG = 1,      // GNMR / alpha > 1
@@ -54,8 +62,10 @@ struct UpdateArgs {
   uint64_t* keys;                // [U], candidate key or 0
   uint8_t* flags;
   uint8_t* mask;                 // [U], A_{t-1} on entry; cleared for units outside C_t
-  int32_t* counters;             // [kNumCounters], zero on entry
-  int32_t* cand_list;            // [U], members of C_t (any order), counters[kCntCand] of them
+  int32_t* counters;             // [kCounterSets][kNumCounters], zero on entry
+  int32_t* cand_list;            // [kCounterSets][list_cap]: set j holds counters[j][kCntCand]
+                                 // members of C_t (any order)
+  int64_t list_cap;              // entries per set of cand_list
   double* gsum;                  // [U], sum of GNMR over the static baseline's profiling steps
 };
 
@@ -67,8 +77,10 @@ struct SelectArgs {
   int64_t* step;       // steps completed (device); advanced by one at the end of K3
   const uint8_t* flags;
   const uint64_t* keys;
-  int32_t* counters;         // from K2; reset to zero for the next step
-  const int32_t* cand_list;  // from K2
+  int32_t* counters;         // from K2, [num_sets][kNumCounters]; reset to zero for the next step
+  const int32_t* cand_list;  // from K2, [num_sets][list_cap]
+  int32_t num_sets;          // kCounterSets (one in the single-workgroup kernel)
+  int64_t list_cap;
   int32_t* lock;       // in: Lock after step t-1; out: after step t
   uint8_t* mask;
   gnmr_stats* stats;

@@ -264,6 +264,7 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, const float* 
   u.mask = c->d_mask;
   u.counters = c->d_counters;
   u.cand_list = c->d_cand_list;
+  u.list_cap = gnmr::cand_list_cap(c->U);
   gnmr::SelectArgs s{};
   s.num_units = c->U;
   s.max_o = c->max_o;
@@ -274,6 +275,8 @@ gnmr_status update_and_select(gnmr_ctx* c, const double* ext_norm, const float* 
   s.keys = c->d_keys;
   s.counters = c->d_counters;
   s.cand_list = c->d_cand_list;
+  s.num_sets = gnmr::kCounterSets;
+  s.list_cap = u.list_cap;
   s.lock = c->d_lock;
   s.mask = c->d_mask;
   s.stats = c->d_stats;
@@ -424,8 +427,9 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   const size_t o_fl = take(size_t(U));
   const size_t o_mask = take(size_t(U));
   const size_t o_keys = take(size_t(U) * sizeof(uint64_t));
-  const size_t o_cnt = take(gnmr::kNumCounters * sizeof(int32_t));
-  const size_t o_list = take(size_t(U) * sizeof(int32_t));
+  const size_t o_cnt = take(size_t(gnmr::kCounterSets) * gnmr::kNumCounters * sizeof(int32_t));
+  const size_t o_list =
+      take(size_t(gnmr::kCounterSets) * size_t(gnmr::cand_list_cap(U)) * sizeof(int32_t));
   const size_t o_gsum = take(size_t(U) * sizeof(double));
   const size_t o_st = take(sizeof(gnmr_stats));
   const size_t o_step = take(sizeof(int64_t));
@@ -500,7 +504,8 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   if (e == hipSuccess) e = hipMemsetAsync(c->d_stats, 0, sizeof(gnmr_stats), st);
   if (e == hipSuccess) e = hipMemsetAsync(c->d_step, 0, sizeof(int64_t), st);
   if (e == hipSuccess)
-    e = hipMemsetAsync(c->d_counters, 0, gnmr::kNumCounters * sizeof(int32_t), st);
+    e = hipMemsetAsync(c->d_counters, 0,
+                       size_t(gnmr::kCounterSets) * gnmr::kNumCounters * sizeof(int32_t), st);
   if (e == hipSuccess && S > 0)
     e = hipMemsetAsync(c->d_seg_base, 0, size_t(S) * sizeof(void*), st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);

@@ -74,12 +74,14 @@ __device__ __forceinline__ uint64_t cand_key(double R) {
   return uint64_t(__double_as_longlong(R)) + 1;
 }
 
+// What one unit adds to the step's counters and candidate list.
+struct Contrib {
+  bool cand, ranked, tg, td, tr, nonfinite;
+};
+
 // Alg. 1 and the risk of Alg. 2 for unit b given its norm n, and the unit's
-// membership of the candidate pool C_t.  kWaveAgg: every lane of the
-// wavefront handles its own unit and the counters are aggregated by ballot;
-// otherwise one lane calls this for its unit alone.
-template <bool kWaveAgg>
-__device__ __forceinline__ void update_unit(const UpdateArgs& a, int b, double n) {
+// membership of the candidate pool C_t; returns what it adds to the counters.
+__device__ __forceinline__ Contrib update_unit(const UpdateArgs& a, int b, double n) {
   const int U = a.num_units;
   // The step counter lives on the device, so that a captured step replays
   // correctly: t = 1 + steps completed, the queue holds min(t - 1, delta)
@@ -153,34 +155,46 @@ __device__ __forceinline__ void update_unit(const UpdateArgs& a, int b, double n
     a.mask[b] = 0;
     if (a.lock[b] != 0) a.lock[b] = 0;
   }
-  // Counters and the list of C_t (integer atomics: exact; list order is
-  // irrelevant to the selection).
-  if constexpr (kWaveAgg) {
-    const uint64_t active = __ballot(1);
-    const int leader = __ffsll((unsigned long long)active) - 1;
-    const int wl = threadIdx.x & 63;
-    const uint64_t m_c = __ballot(cand);
-    const uint64_t m_g = __ballot(tg), m_d = __ballot(td), m_r = __ballot(tr);
-    const uint64_t m_n = __ballot(!finite), m_k = __ballot(ranked);
-    int base = 0;
-    if (wl == leader) {
-      if (m_c) base = atomicAdd(&a.counters[kCntCand], __popcll(m_c));
-      if (m_k) atomicAdd(&a.counters[kCntRank], __popcll(m_k));
-      if (m_g) atomicAdd(&a.counters[kCntTrigG], __popcll(m_g));
-      if (m_d) atomicAdd(&a.counters[kCntTrigD], __popcll(m_d));
-      if (m_r) atomicAdd(&a.counters[kCntTrigR], __popcll(m_r));
-      if (m_n) atomicAdd(&a.counters[kCntNonFinite], __popcll(m_n));
-    }
-    base = __shfl(base, leader, 64);
-    if (cand) a.cand_list[base + __popcll(m_c & ((uint64_t(1) << wl) - 1))] = b;
-  } else {
-    if (cand) a.cand_list[atomicAdd(&a.counters[kCntCand], 1)] = b;
-    if (ranked) atomicAdd(&a.counters[kCntRank], 1);
-    if (tg) atomicAdd(&a.counters[kCntTrigG], 1);
-    if (td) atomicAdd(&a.counters[kCntTrigD], 1);
-    if (tr) atomicAdd(&a.counters[kCntTrigR], 1);
-    if (!finite) atomicAdd(&a.counters[kCntNonFinite], 1);
+  return Contrib{cand, ranked, tg, td, tr, !finite};
+}
+
+// Adds the contributions of a workgroup's units (`has`: this thread holds
+// unit b) to counter set blockIdx.x % kCounterSets and appends its members
+// of C_t to that set's list: summed by ballot and LDS first, then one global
+// atomic per counter and workgroup (integer atomics: exact; the list order
+// is irrelevant to the selection).  Called by every thread of the workgroup.
+__device__ void publish(const UpdateArgs& a, bool has, int b, const Contrib& c) {
+  __shared__ int32_t s_cnt[kNumCounters];
+  __shared__ int32_t s_base;
+  const int tid = int(threadIdx.x), wl = tid & 63;
+  if (tid < kNumCounters) s_cnt[tid] = 0;
+  __syncthreads();
+  const uint64_t m_c = __ballot(has && c.cand);
+  const uint64_t m_k = __ballot(has && c.ranked), m_g = __ballot(has && c.tg);
+  const uint64_t m_d = __ballot(has && c.td), m_r = __ballot(has && c.tr);
+  const uint64_t m_n = __ballot(has && c.nonfinite);
+  int wave_base = 0;
+  if (wl == 0) {
+    if (m_c) wave_base = atomicAdd(&s_cnt[kCntCand], __popcll(m_c));
+    if (m_k) atomicAdd(&s_cnt[kCntRank], __popcll(m_k));
+    if (m_g) atomicAdd(&s_cnt[kCntTrigG], __popcll(m_g));
+    if (m_d) atomicAdd(&s_cnt[kCntTrigD], __popcll(m_d));
+    if (m_r) atomicAdd(&s_cnt[kCntTrigR], __popcll(m_r));
+    if (m_n) atomicAdd(&s_cnt[kCntNonFinite], __popcll(m_n));
   }
+  wave_base = __shfl(wave_base, 0, 64);
+  const int slot = wave_base + __popcll(m_c & ((uint64_t(1) << wl) - 1));
+  __syncthreads();
+  const int set = int(blockIdx.x % kCounterSets);
+  if (tid == 0) {
+    int32_t* cs = a.counters + set * kNumCounters;
+    s_base = s_cnt[kCntCand] ? atomicAdd(&cs[kCntCand], s_cnt[kCntCand]) : 0;
+#pragma unroll
+    for (int k = 1; k < kNumCounters; ++k)
+      if (s_cnt[k]) atomicAdd(&cs[k], s_cnt[k]);
+  }
+  __syncthreads();
+  if (has && c.cand) a.cand_list[set * a.list_cap + s_base + slot] = b;
 }
 
 // K2: L lanes per unit sum its partials; lane 0 then runs Alg. 1, the risk of
@@ -190,19 +204,25 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
   __shared__ double red[4];
   const int lane = L == 1 ? 0 : int(threadIdx.x % L);
   const int b = blockIdx.x * (256 / L) + threadIdx.x / L;
-  if (b >= a.num_units) return;  // uniform per workgroup when L = 256
-  double n;
-  if (a.ext_norm != nullptr) {
-    n = a.ext_norm[b];
-  } else {
-    n = sqrt(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
+  if (L == 256 && b >= a.num_units) return;  // the whole workgroup
+  const bool in = b < a.num_units;           // uniform per wavefront when L = 64
+  double n = 0.0;
+  if (in) {
+    if (a.ext_norm != nullptr) {
+      n = a.ext_norm[b];
+    } else {
+      n = sqrt(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
+    }
   }
-  if (lane != 0) return;
-  update_unit<L == 1>(a, b, n);
+  const bool has = in && lane == 0;
+  Contrib c{};
+  if (has) c = update_unit(a, b, n);
+  publish(a, has, b, c);
 }
 
 constexpr int kK3Block = 1024;
-constexpr int kK3Cap = 4096;  // candidates held in LDS; larger pools use the global keys
+constexpr int kK3Cap = 12288;  // candidates held in LDS (144 KiB); larger pools use the global keys
+constexpr int kK3Count = 128;  // pools up to this size are ranked by direct counting
 
 // Lock update of Alg. 2 for one unit given its selection.
 __device__ __forceinline__ void apply_selection(const SelectArgs& a, int b, bool sel, uint8_t f) {
@@ -227,9 +247,28 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += kK3Block) {
-      const uint64_t key = key_at(i);
-      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    // In the upper bytes of R's bits the keys of a wavefront mostly share
+    // one digit: then one lane adds them all (one LDS atomic, not one per key
+    // on the same counter); otherwise every key adds itself.
+    const int rounds = (n + kK3Block - 1) / kK3Block;
+    for (int r = 0; r < rounds; ++r) {
+      const int i = tid + r * kK3Block;
+      bool pend = false;
+      uint32_t d = 0;
+      if (i < n) {
+        const uint64_t key = key_at(i);
+        pend = (key & pmask) == prefix;
+        d = uint32_t(key >> shift) & 255u;
+      }
+      const uint64_t m = __ballot(pend);
+      if (m == 0) continue;
+      const int leader = __ffsll((unsigned long long)m) - 1;
+      const uint32_t dl = __shfl(d, leader, 64);
+      if (__ballot(pend && d == dl) == m) {
+        if ((tid & 63) == leader) atomicAdd(&hist[dl], uint32_t(__popcll(m)));
+      } else if (pend) {
+        atomicAdd(&hist[d], 1u);
+      }
     }
     __syncthreads();
     if (tid < 64) {
@@ -327,9 +366,9 @@ __device__ void bitonic_sort(int32_t* v) {
 // K3: a single workgroup, over the members of C_t listed by K2.  Kept units
 // (warm-up; continuing units under the admitted-only budget) are active
 // without ranking; the others are ranked for the budget.  When at most maxO
-// are ranked they are all active.  Otherwise pools of at most one candidate
-// per thread count each candidate's place in the order directly; larger
-// ones need the maxO-th largest ranked key T (radix select; kept units carry
+// are ranked they are all active.  Otherwise small pools (up to kK3Count)
+// count each candidate's place in the order directly; larger ones need the
+// maxO-th largest ranked key T (radix select; kept units carry
 // key 0): every ranked candidate with key > T is active, and the first
 // `need` with key == T in index order.  Pools of up to kK3Cap candidates are
 // ranked in LDS; larger ones over the global keys of all units.
@@ -343,31 +382,66 @@ __device__ void select_body(const SelectArgs& a) {
   uint32_t* scan = reinterpret_cast<uint32_t*>(tie_idx);  // the global path reuses it
   const int tid = threadIdx.x;
   const int U = a.num_units;
-  const int n_cand = a.counters[kCntCand];
-  const int n_rank = a.counters[kCntRank];
+  // Gather K2's counter sets: totals, and where each set's candidates start
+  // in the pool's order (one wavefront, lane j holding set j).
+  __shared__ int32_t s_tot[kNumCounters];
+  __shared__ int32_t s_setoff[kCounterSets + 1];
+  static_assert(kCounterSets == 64, "one lane per counter set");
+  if (tid < 64) {
+    const bool have = tid < a.num_sets;
+    int32_t v[kNumCounters];
+#pragma unroll
+    for (int k = 0; k < kNumCounters; ++k) v[k] = have ? a.counters[tid * kNumCounters + k] : 0;
+    int32_t inc = v[kCntCand];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t w = __shfl_up(inc, off, 64);
+      if (tid >= off) inc += w;
+    }
+    s_setoff[tid + 1] = inc;
+    if (tid == 0) s_setoff[0] = 0;
+#pragma unroll
+    for (int k = 0; k < kNumCounters; ++k) {
+      int32_t t = v[k];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) t += __shfl_xor(t, m, 64);
+      if (tid == 0) s_tot[k] = t;
+    }
+  }
   if (tid < 2) cnt[tid] = 0;
   __syncthreads();
+  const int n_cand = s_tot[kCntCand];
+  const int n_rank = s_tot[kCntRank];
+  // the i-th candidate of the pool: set j with s_setoff[j] <= i < s_setoff[j+1]
+  auto cand_at = [&](int i) {
+    int lo = 0, hi = a.num_sets;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_setoff[mid] <= i) lo = mid; else hi = mid;
+    }
+    return a.cand_list[lo * a.list_cap + (i - s_setoff[lo])];
+  };
 
   int c_act = 0;
   if (a.max_o == 0 || n_rank <= a.max_o) {
     // no ranking: every listed unit is active, or only the kept ones if maxO = 0
     const bool take = a.max_o > 0;
     for (int i = tid; i < n_cand; i += kK3Block) {
-      const int b = a.cand_list[i];
+      const int b = cand_at(i);
       const uint8_t f = a.flags[b];
       const bool sel = take || (f & kFlagKeep);
       apply_selection(a, b, sel, f);
       c_act += sel;
     }
-  } else if (n_cand <= kK3Block) {
-    // A pool of at most one candidate per thread: each ranked candidate's
-    // place in the order (R descending, index ascending) is counted
-    // directly against the whole pool, one barrier instead of the radix
-    // passes.  Kept units carry key 0, below every ranked key, so they never
-    // push a ranked one down; a ranked candidate is active when fewer than
-    // maxO candidates come before it.
+  } else if (n_cand <= kK3Count) {
+    // A small pool: each ranked candidate's place in the order (R
+    // descending, index ascending) is counted directly against the whole
+    // pool, one barrier instead of the radix passes.  Kept units carry key
+    // 0, below every ranked key, so they never push a ranked one down; a
+    // ranked candidate is active when fewer than maxO candidates come before
+    // it.
     if (tid < n_cand) {
-      const int b = a.cand_list[tid];
+      const int b = cand_at(tid);
       c_idx[tid] = b;
       c_key[tid] = a.keys[b];
     }
@@ -376,7 +450,8 @@ __device__ void select_body(const SelectArgs& a) {
       const int b = c_idx[tid];
       const uint64_t key = c_key[tid];
       int before = 0;
-      for (int j = 0; j < n_cand && before < a.max_o; ++j) {
+#pragma unroll 8
+      for (int j = 0; j < n_cand; ++j) {
         const uint64_t kj = c_key[j];
         before += (kj > key || (kj == key && c_idx[j] < b)) ? 1 : 0;
       }
@@ -393,7 +468,7 @@ __device__ void select_body(const SelectArgs& a) {
     c_act = select_by_scan(a, T, need, scan);
   } else {
     for (int i = tid; i < n_cand; i += kK3Block) {
-      const int b = a.cand_list[i];
+      const int b = cand_at(i);
       c_idx[i] = b;
       c_key[i] = a.keys[b];
     }
@@ -437,18 +512,19 @@ __device__ void select_body(const SelectArgs& a) {
     const bool warm = t <= a.warmup;
     gnmr_stats st;
     st.t = t;
-    st.n_trig_gnmr = a.counters[kCntTrigG];
-    st.n_trig_dgnmr = a.counters[kCntTrigD];
-    st.n_trig = a.counters[kCntTrigR];
+    st.n_trig_gnmr = s_tot[kCntTrigG];
+    st.n_trig_dgnmr = s_tot[kCntTrigD];
+    st.n_trig = s_tot[kCntTrigR];
     st.n_cand = n_cand;
     st.n_active = cnt[0];
     st.hit_maxo = (!warm && n_rank > 0 && n_rank >= a.max_o) ? 1 : 0;
-    st.n_nonfinite = a.counters[kCntNonFinite];
+    st.n_nonfinite = s_tot[kCntNonFinite];
     st.reserved = 0;
     *a.stats = st;
-    for (int k = 0; k < kNumCounters; ++k) a.counters[k] = 0;  // ready for the next step
     *a.step = t;
   }
+  // the counter sets, ready for the next step (read only in the gather above)
+  for (int k = tid; k < a.num_sets * kNumCounters; k += kK3Block) a.counters[k] = 0;
 }
 
 __global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) { select_body(a); }
@@ -464,17 +540,22 @@ __global__ __launch_bounds__(kK3Block) void k23_small(UpdateArgs u, SelectArgs s
   __shared__ int32_t s_counters[kNumCounters];
   __shared__ int32_t s_cand[kK3Block];
   if (threadIdx.x < kNumCounters) s_counters[threadIdx.x] = 0;
+  // one counter set, in LDS
   u.counters = s.counters = s_counters;
   u.cand_list = s_cand;
   s.cand_list = s_cand;
-  __syncthreads();
+  u.list_cap = s.list_cap = kK3Block;
+  s.num_sets = 1;
   const int b = int(threadIdx.x);
-  if (b < u.num_units) {
+  const bool has = b < u.num_units;
+  Contrib c{};
+  if (has) {
     const double n = u.ext_norm != nullptr
                          ? u.ext_norm[b]
                          : sqrt(unit_ss<1>(u.unit_item_off, u.partial, b, 0, nullptr));
-    update_unit<true>(u, b, n);
+    c = update_unit(u, b, n);
   }
+  publish(u, has, b, c);  // its first barrier also orders the clear above
   __syncthreads();
   select_body(s);
 }

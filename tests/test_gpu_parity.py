@@ -285,22 +285,38 @@ def test_abi_errors_leave_state_unchanged():
         assert ctl.query()["stats"]["t"] == 2
 
 
-@pytest.mark.parametrize("case", ["few_ties_at_cut", "mid_pool_ties_at_cut", "many_ties_at_cut",
-                                  "huge_pool", "pool_at_capacity", "pool_of_one_per_thread"])
+@pytest.mark.parametrize("case", ["small_pool_ties_at_cut", "pool_at_count_limit",
+                                  "pool_over_count_limit", "few_ties_at_cut",
+                                  "mid_pool_ties_at_cut", "many_ties_at_cut", "pool_at_capacity",
+                                  "huge_pool"])
 def test_selection_paths(case):
-    """Top_maxO through each selection path of the kernel: a pool of at most
-    one candidate per thread ranked by direct counting, with index-ordered
-    ties at the cut (few_ties_at_cut) and at exactly 1,024 candidates; larger
-    pools by radix select in LDS with the ties at the cut sorted
-    (mid_pool_ties_at_cut), more ties than the tie buffer, more candidates
-    than the LDS pool (global keys), and a pool right at it."""
+    """Top_maxO through each selection path of the kernel: small pools (up
+    to 128 candidates) ranked by direct counting, with index-ordered ties at
+    the cut and at the size limit; larger pools by radix select in LDS, with
+    the ties at the cut sorted (few_ties_at_cut, mid_pool_ties_at_cut), with
+    more ties than the tie buffer, and right at the LDS pool's capacity
+    (12,288); more candidates than that over the global keys."""
     torch = require_gpu()
     from paper_2606_00539_amd import Controller
 
     rng = np.random.default_rng(11)
     U, T, max_o, alpha = 3000, 12, 64, 1.1
     base = np.exp(rng.normal(scale=0.05, size=(T, U)))
-    if case == "few_ties_at_cut":
+    if case == "small_pool_ties_at_cut":
+        # 100 candidates: 20 distinct spikes, a 60-unit tie holding the cut,
+        # 20 weaker spikes below it
+        perm = rng.permutation(U)
+        base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
+        tied, strong, weak = perm[:60], perm[60:80], perm[80:100]
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+        base[9, strong] *= 18.0 + np.arange(20)
+        base[9, weak] *= 2.0
+    elif case in ("pool_at_count_limit", "pool_over_count_limit"):
+        n = 128 if case == "pool_at_count_limit" else 129
+        base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
+        base[9, rng.permutation(U)[:n]] *= 6.0 + rng.random(n)
+    elif case == "few_ties_at_cut":
         # 300 units share one norm stream and spike together; 20 spike harder
         tied = rng.choice(U, 300, replace=False)
         base[:, tied] = base[:, tied[:1]]
@@ -316,22 +332,18 @@ def test_selection_paths(case):
         base[9, tied] *= 6.0
         base[9, strong] *= 18.0 + np.arange(20)
         base[9, weak] *= 2.0
-    elif case == "pool_of_one_per_thread":
-        U = 3000
-        base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
-        base[9, :1024] *= 6.0 + rng.random(1024)   # exactly 1,024 candidates at t = 10
     elif case == "many_ties_at_cut":
         tied = rng.choice(U, 1500, replace=False)
         base[:, tied] = base[:, tied[:1]]
         base[9, tied] *= 6.0
     elif case == "huge_pool":
-        U = 10000
+        U = 14000
         base = np.exp(rng.normal(scale=0.05, size=(T, U)))
-        alpha = 0.4                                # every unit triggers: |C_t| = U > 4096
+        alpha = 0.4                                # every unit triggers: |C_t| = U > 12,288
     elif case == "pool_at_capacity":
-        U = 5000
+        U = 13000
         base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
-        base[9, :4096] *= 6.0                      # exactly 4096 candidates at t = 10
+        base[9, :12288] *= 6.0                     # exactly 12,288 candidates at t = 10
     ora = Oracle(U, window=5, max_o=max_o, lock_len=2, eps=1e-12)
     dn = torch.empty(U, dtype=torch.float64, device="cuda")
     say("selection path:", case, "units", U)
@@ -341,12 +353,13 @@ def test_selection_paths(case):
             ctl.step_from_norms(dn, alpha, 1.5)
             ref = ora.step(base[t - 1], alpha, 1.5)
             assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} t={t}")
-            if case == "pool_at_capacity" and t == 10:
-                assert ref.stats["n_cand"] == 4096
-            if case == "pool_of_one_per_thread" and t == 10:
-                assert ref.stats["n_cand"] == 1024
-            if case == "mid_pool_ties_at_cut" and t == 10:
-                assert 1024 < ref.stats["n_cand"] <= 4096
+            if t == 10:
+                want = {"pool_at_capacity": 12288, "pool_at_count_limit": 128,
+                        "pool_over_count_limit": 129, "small_pool_ties_at_cut": 100}
+                if case in want:
+                    assert ref.stats["n_cand"] == want[case]
+                if case == "mid_pool_ties_at_cut":
+                    assert 128 < ref.stats["n_cand"] <= 12288
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama2-13b", "moe", "fine32"])
