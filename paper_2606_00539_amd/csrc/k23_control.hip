@@ -238,15 +238,21 @@ __device__ __forceinline__ void apply_selection(const SelectArgs& a, int b, bool
 // MSB-first radix select, 8 passes of 8 bits: the k-th largest (1-based) of
 // the n keys key_at(i), i < n.  Returns it as T; *rest receives how many keys
 // equal to T are among the k largest.  Called by every thread of the
-// workgroup.
+// workgroup.  Two barriers per pass: the histograms alternate between the
+// two halves of hist[512], so a pass clears the next pass's half (last read
+// before the previous pass's second barrier) while it counts into its own,
+// and the digit it publishes is read by every thread before any thread can
+// reach the barrier after which the next digit is written.
 template <typename KeyAt>
 __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int* s_digit,
                                  int* s_k, int* rest) {
   const int tid = threadIdx.x;
   uint64_t prefix = 0, pmask = 0;
-  for (int shift = 56; shift >= 0; shift -= 8) {
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
+  if (tid < 256) hist[tid] = 0;
+  __syncthreads();
+  for (int shift = 56, pass = 0; shift >= 0; shift -= 8, ++pass) {
+    uint32_t* const h = hist + (pass & 1) * 256;
+    if (tid < 256) hist[((pass + 1) & 1) * 256 + tid] = 0;
     // In the upper bytes of R's bits the keys of a wavefront mostly share
     // one digit: then one lane adds them all (one LDS atomic, not one per key
     // on the same counter); otherwise every key adds itself.
@@ -265,9 +271,9 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
       const int leader = __ffsll((unsigned long long)m) - 1;
       const uint32_t dl = __shfl(d, leader, 64);
       if (__ballot(pend && d == dl) == m) {
-        if ((tid & 63) == leader) atomicAdd(&hist[dl], uint32_t(__popcll(m)));
+        if ((tid & 63) == leader) atomicAdd(&h[dl], uint32_t(__popcll(m)));
       } else if (pend) {
-        atomicAdd(&hist[d], 1u);
+        atomicAdd(&h[d], 1u);
       }
     }
     __syncthreads();
@@ -278,8 +284,7 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
       // each lane's digits, and the one lane whose digits reach k names d
       // (k <= the keys in the histogram, so exactly one lane does).
       const int l = tid;
-      const uint32_t h0 = hist[4 * l], h1 = hist[4 * l + 1], h2 = hist[4 * l + 2],
-                     h3 = hist[4 * l + 3];
+      const uint32_t h0 = h[4 * l], h1 = h[4 * l + 1], h2 = h[4 * l + 2], h3 = h[4 * l + 3];
       const uint32_t own = h0 + h1 + h2 + h3;
       uint32_t suffix = own;  // keys with a digit >= 4l
 #pragma unroll
@@ -291,8 +296,8 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
       const uint32_t uk = uint32_t(k);
       if (above < uk && above + own >= uk) {
         int d = 4 * l + 3;
-        const uint32_t h[4] = {h0, h1, h2, h3};
-        for (int j = 3; j > 0 && above + h[j] < uk; --j, --d) above += h[j];
+        const uint32_t hv[4] = {h0, h1, h2, h3};
+        for (int j = 3; j > 0 && above + hv[j] < uk; --j, --d) above += hv[j];
         *s_digit = d;
         *s_k = k - int(above);
       }
@@ -301,7 +306,6 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
     prefix |= uint64_t(*s_digit) << shift;
     pmask |= uint64_t(255) << shift;
     k = *s_k;
-    __syncthreads();
   }
   *rest = k;
   return prefix;
@@ -376,7 +380,7 @@ __device__ void select_body(const SelectArgs& a) {
   __shared__ uint64_t c_key[kK3Cap];
   __shared__ int32_t c_idx[kK3Cap];
   __shared__ int32_t tie_idx[kK3Block];
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[2 * 256];
   __shared__ int cnt[2];  // active, ties
   __shared__ int s_digit, s_k;
   uint32_t* scan = reinterpret_cast<uint32_t*>(tie_idx);  // the global path reuses it
