@@ -197,6 +197,29 @@ __device__ void publish(const UpdateArgs& a, bool has, int b, const Contrib& c) 
   if (has && c.cand) a.cand_list[set * a.list_cap + s_base + slot] = b;
 }
 
+// The same for a kernel of one workgroup whose counters and list are in LDS:
+// one LDS atomic per counter and wavefront, no barrier (the caller's next
+// barrier makes the results visible).
+__device__ __forceinline__ void publish_local(int32_t* cnt, int32_t* list, bool has, int b,
+                                              const Contrib& c) {
+  const int wl = int(threadIdx.x & 63);
+  const uint64_t m_c = __ballot(has && c.cand);
+  const uint64_t m_k = __ballot(has && c.ranked), m_g = __ballot(has && c.tg);
+  const uint64_t m_d = __ballot(has && c.td), m_r = __ballot(has && c.tr);
+  const uint64_t m_n = __ballot(has && c.nonfinite);
+  int base = 0;
+  if (wl == 0) {
+    if (m_c) base = atomicAdd(&cnt[kCntCand], __popcll(m_c));
+    if (m_k) atomicAdd(&cnt[kCntRank], __popcll(m_k));
+    if (m_g) atomicAdd(&cnt[kCntTrigG], __popcll(m_g));
+    if (m_d) atomicAdd(&cnt[kCntTrigD], __popcll(m_d));
+    if (m_r) atomicAdd(&cnt[kCntTrigR], __popcll(m_r));
+    if (m_n) atomicAdd(&cnt[kCntNonFinite], __popcll(m_n));
+  }
+  base = __shfl(base, 0, 64);
+  if (has && c.cand) list[base + __popcll(m_c & ((uint64_t(1) << wl) - 1))] = b;
+}
+
 // K2: L lanes per unit sum its partials; lane 0 then runs Alg. 1, the risk of
 // Alg. 2, and marks the unit's membership of the candidate pool C_t.
 template <int L>
@@ -374,11 +397,12 @@ __device__ void bitonic_sort(int32_t* v) {
 // count each candidate's place in the order directly; larger ones need the
 // maxO-th largest ranked key T (radix select; kept units carry
 // key 0): every ranked candidate with key > T is active, and the first
-// `need` with key == T in index order.  Pools of up to kK3Cap candidates are
+// `need` with key == T in index order.  Pools of up to kCap candidates are
 // ranked in LDS; larger ones over the global keys of all units.
+template <int kCap>
 __device__ void select_body(const SelectArgs& a) {
-  __shared__ uint64_t c_key[kK3Cap];
-  __shared__ int32_t c_idx[kK3Cap];
+  __shared__ uint64_t c_key[kCap];
+  __shared__ int32_t c_idx[kCap];
   __shared__ int32_t tie_idx[kK3Block];
   __shared__ uint32_t hist[2 * 256];
   __shared__ int cnt[2];  // active, ties
@@ -387,32 +411,25 @@ __device__ void select_body(const SelectArgs& a) {
   const int tid = threadIdx.x;
   const int U = a.num_units;
   // Gather K2's counter sets: totals, and where each set's candidates start
-  // in the pool's order (one wavefront, lane j holding set j).
+  // in the pool's order (one thread per counter, then one for the offsets).
+  __shared__ int32_t s_sets[kCounterSets * kNumCounters];
   __shared__ int32_t s_tot[kNumCounters];
   __shared__ int32_t s_setoff[kCounterSets + 1];
-  static_assert(kCounterSets == 64, "one lane per counter set");
-  if (tid < 64) {
-    const bool have = tid < a.num_sets;
-    int32_t v[kNumCounters];
-#pragma unroll
-    for (int k = 0; k < kNumCounters; ++k) v[k] = have ? a.counters[tid * kNumCounters + k] : 0;
-    int32_t inc = v[kCntCand];
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int32_t w = __shfl_up(inc, off, 64);
-      if (tid >= off) inc += w;
-    }
-    s_setoff[tid + 1] = inc;
-    if (tid == 0) s_setoff[0] = 0;
-#pragma unroll
-    for (int k = 0; k < kNumCounters; ++k) {
-      int32_t t = v[k];
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) t += __shfl_xor(t, m, 64);
-      if (tid == 0) s_tot[k] = t;
+  if (tid < a.num_sets * kNumCounters) s_sets[tid] = a.counters[tid];
+  if (tid < 2) cnt[tid] = 0;
+  __syncthreads();
+  if (tid < kNumCounters) {
+    int32_t t = 0;
+    for (int j = 0; j < a.num_sets; ++j) t += s_sets[j * kNumCounters + tid];
+    s_tot[tid] = t;
+  } else if (tid == kNumCounters) {
+    int32_t t = 0;
+    s_setoff[0] = 0;
+    for (int j = 0; j < a.num_sets; ++j) {
+      t += s_sets[j * kNumCounters + kCntCand];
+      s_setoff[j + 1] = t;
     }
   }
-  if (tid < 2) cnt[tid] = 0;
   __syncthreads();
   const int n_cand = s_tot[kCntCand];
   const int n_rank = s_tot[kCntRank];
@@ -464,7 +481,7 @@ __device__ void select_body(const SelectArgs& a) {
       apply_selection(a, b, sel, f);
       c_act += sel;
     }
-  } else if (n_cand > kK3Cap) {
+  } else if (n_cand > kCap) {
     int need = 0;
     const uint64_t* __restrict__ keys = a.keys;
     const uint64_t T = radix_select([=](int i) { return keys[i]; }, U, a.max_o, hist, &s_digit,
@@ -531,7 +548,7 @@ __device__ void select_body(const SelectArgs& a) {
   for (int k = tid; k < a.num_sets * kNumCounters; k += kK3Block) a.counters[k] = 0;
 }
 
-__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) { select_body(a); }
+__global__ __launch_bounds__(kK3Block) void k3_select(SelectArgs a) { select_body<kK3Cap>(a); }
 
 // K2 and K3 in one workgroup, for small workloads: at most kK3Block units,
 // each summed by one thread exactly as k2_update<1> sums it (or given its
@@ -550,6 +567,7 @@ __global__ __launch_bounds__(kK3Block) void k23_small(UpdateArgs u, SelectArgs s
   s.cand_list = s_cand;
   u.list_cap = s.list_cap = kK3Block;
   s.num_sets = 1;
+  __syncthreads();
   const int b = int(threadIdx.x);
   const bool has = b < u.num_units;
   Contrib c{};
@@ -559,9 +577,9 @@ __global__ __launch_bounds__(kK3Block) void k23_small(UpdateArgs u, SelectArgs s
                          : sqrt(unit_ss<1>(u.unit_item_off, u.partial, b, 0, nullptr));
     c = update_unit(u, b, n);
   }
-  publish(u, has, b, c);  // its first barrier also orders the clear above
+  publish_local(s_counters, s_cand, has, b, c);
   __syncthreads();
-  select_body(s);
+  select_body<kK3Block>(s);  // at most kK3Block units, so the pool fits
 }
 
 }  // namespace
