@@ -127,6 +127,22 @@ def cpu_baseline_all_cores(buf, lay, w, single_gbs: float, target_s: float = 10.
                       f"({total / 1e9:.1f} GB, {spent:.1f} s)"}
 
 
+def event_time(torch, fn, reps: int, stream=None, lead_in: int = 1) -> float:
+    """Average ms of fn() over `reps` calls between two events on `stream`.
+    `lead_in` untimed calls are queued right before the first event, with no
+    synchronisation in between, so that the device is busy when the event is
+    reached and a host delay before the first timed call is not counted."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(lead_in):
+        fn()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
 def library_reduce_probe(torch, buf, lay, w, reps: int = 5):
     """torch.linalg.vector_norm over the same gradient bytes viewed as one
     flat tensor of the workload's dtype: the library's own read-reduce, as a
@@ -136,16 +152,7 @@ def library_reduce_probe(torch, buf, lay, w, reps: int = 5):
         return None
     dt = torch.bfloat16 if dts.pop() == 1 else torch.float32
     x = buf[:w.bytes_per_step].view(dt)
-    for _ in range(2):
-        torch.linalg.vector_norm(x)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        torch.linalg.vector_norm(x)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    ms = event_time(torch, lambda: torch.linalg.vector_norm(x), reps, lead_in=2)
     return {"kind": "torch.linalg.vector_norm over the same bytes", "ms": round(ms, 4),
             "GBs": round(w.bytes_per_step / (ms * 1e-3) / 1e9, 1)}
 
@@ -162,16 +169,8 @@ def read_ceiling_probe(torch, buf, w, stream, reps: int = 5):
     for v, name in rp.VARIANTS.items():
         parts = torch.empty(rp.num_partials(w.bytes_per_step, v), dtype=torch.float32,
                             device="cuda")
-        for _ in range(2):
-            rp.run(buf.data_ptr(), w.bytes_per_step, parts.data_ptr(), v, s)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(reps):
-            rp.run(buf.data_ptr(), w.bytes_per_step, parts.data_ptr(), v, s)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / reps
+        ms = event_time(torch, lambda: rp.run(buf.data_ptr(), w.bytes_per_step,
+                                              parts.data_ptr(), v, s), reps, stream, lead_in=2)
         out[name] = {"ms": round(ms, 4), "GBs": round(w.bytes_per_step / (ms * 1e-3) / 1e9, 1)}
     return out
 
@@ -241,16 +240,8 @@ def actuator_bench(torch, tokens: int, steps: int, warmup: int) -> None:
         mask = np.zeros(U, np.uint8)
         mask[np.random.default_rng(0).choice(U, nrec, replace=False)] = 1
         d_mask = torch.from_numpy(mask).to("cuda")
-        for _ in range(warmup):
-            act.apply(d_mask, GNMR_FMT_E2M1, GNMR_FMT_BF16)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(steps):
-            act.apply(d_mask, GNMR_FMT_E2M1, GNMR_FMT_BF16)
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
+        ms = event_time(torch, lambda: act.apply(d_mask, GNMR_FMT_E2M1, GNMR_FMT_BF16), steps,
+                        lead_in=max(warmup, 1))
         moved = 2 * sum(r * c * 2 for (r, c), m in zip(shapes, mask) if not m)
         results[label] = {"ms": round(ms, 4), "bytes_moved": moved,
                           "GBs": round(moved / (ms * 1e-3) / 1e9, 1)}
@@ -261,16 +252,8 @@ def actuator_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     rp = ReadProbe()
     dst = torch.empty_like(buf)
     nb = buf.numel() * 2 // 16 * 16
-    for _ in range(2):
-        rp.copy(buf.data_ptr(), dst.data_ptr(), nb)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(5):
-        rp.copy(buf.data_ptr(), dst.data_ptr(), nb)
-    e1.record()
-    torch.cuda.synchronize()
-    copy_ms = e0.elapsed_time(e1) / 5
+    copy_ms = event_time(torch, lambda: rp.copy(buf.data_ptr(), dst.data_ptr(), nb), 5,
+                         lead_in=2)
     copy_gbs = 2 * nb / (copy_ms * 1e-3) / 1e9
     del dst
     print(json.dumps({
@@ -347,14 +330,8 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
                 torch.mm(dys[b].t(), xs[b], out=dws[b])
 
     def timed(fn, n):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for k in range(n):
-            fn(k + 1)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n
+        calls = iter(range(1, n + 2))
+        return event_time(torch, lambda: fn(next(calls)), n, stream)
 
     for k in range(warmup):
         fused_step(k + 1)
