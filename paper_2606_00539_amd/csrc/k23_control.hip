@@ -415,19 +415,27 @@ __device__ void select_body(const SelectArgs& a) {
   __shared__ int32_t s_sets[kCounterSets * kNumCounters];
   __shared__ int32_t s_tot[kNumCounters];
   __shared__ int32_t s_setoff[kCounterSets + 1];
-  if (tid < a.num_sets * kNumCounters) s_sets[tid] = a.counters[tid];
   if (tid < 2) cnt[tid] = 0;
-  __syncthreads();
-  if (tid < kNumCounters) {
-    int32_t t = 0;
-    for (int j = 0; j < a.num_sets; ++j) t += s_sets[j * kNumCounters + tid];
-    s_tot[tid] = t;
-  } else if (tid == kNumCounters) {
-    int32_t t = 0;
-    s_setoff[0] = 0;
-    for (int j = 0; j < a.num_sets; ++j) {
-      t += s_sets[j * kNumCounters + kCntCand];
-      s_setoff[j + 1] = t;
+  if (a.num_sets == 1) {  // the single-workgroup kernel: one set, nothing to combine
+    if (tid < kNumCounters) s_tot[tid] = a.counters[tid];
+    if (tid == kNumCounters) {
+      s_setoff[0] = 0;
+      s_setoff[1] = a.counters[kCntCand];
+    }
+  } else {  // (num_sets is the same for the whole workgroup)
+    if (tid < a.num_sets * kNumCounters) s_sets[tid] = a.counters[tid];
+    __syncthreads();
+    if (tid < kNumCounters) {
+      int32_t t = 0;
+      for (int j = 0; j < a.num_sets; ++j) t += s_sets[j * kNumCounters + tid];
+      s_tot[tid] = t;
+    } else if (tid == kNumCounters) {
+      int32_t t = 0;
+      s_setoff[0] = 0;
+      for (int j = 0; j < a.num_sets; ++j) {
+        t += s_sets[j * kNumCounters + kCntCand];
+        s_setoff[j + 1] = t;
+      }
     }
   }
   __syncthreads();
