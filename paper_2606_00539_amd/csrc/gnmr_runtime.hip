@@ -368,6 +368,14 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
                                       " (each segment takes one item per started 64 KiB)");
   }
 
+  // K2 workgroups of 1, 4 or 256 units fill counter set w % kCounterSets:
+  // each set's share of the candidate list must fit its capacity
+  for (const int64_t per_wg : {int64_t(1), int64_t(4), int64_t(256)}) {
+    const int64_t wgs = (U + per_wg - 1) / per_wg;
+    if ((wgs + gnmr::kCounterSets - 1) / gnmr::kCounterSets * per_wg > gnmr::cand_list_cap(U))
+      return fail(GNMR_E_INVALID, "candidate list layout does not fit (internal)");
+  }
+
   gnmr_ctx* c = new (std::nothrow) gnmr_ctx;
   if (c == nullptr) return fail(GNMR_E_NOMEM, "host allocation failed");
   c->U = cfg->num_units;
