@@ -266,9 +266,22 @@ __device__ __forceinline__ void apply_selection(const SelectArgs& a, int b, bool
 // before the previous pass's second barrier) while it counts into its own,
 // and the digit it publishes is read by every thread before any thread can
 // reach the barrier after which the next digit is written.
+//
+// Once the bucket that holds the k-th largest key has at most 64 keys, the
+// passes stop: those keys are gathered into LDS and one wavefront finishes by
+// counting, for each, the keys above it (a typical pool of a few thousand R
+// values gets there after 3 of the 8 passes).
+struct RadixSmall {
+  uint64_t key[64];
+  int n;                  // keys gathered
+  int bucket;             // keys in the chosen bucket (written with the digit)
+  uint64_t T;
+  int rest;
+};
+
 template <typename KeyAt>
 __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int* s_digit,
-                                 int* s_k, int* rest) {
+                                 int* s_k, int* rest, RadixSmall* sm) {
   const int tid = threadIdx.x;
   uint64_t prefix = 0, pmask = 0;
   if (tid < 256) hist[tid] = 0;
@@ -276,6 +289,7 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
   for (int shift = 56, pass = 0; shift >= 0; shift -= 8, ++pass) {
     uint32_t* const h = hist + (pass & 1) * 256;
     if (tid < 256) hist[((pass + 1) & 1) * 256 + tid] = 0;
+    if (tid == 0) sm->n = 0;
     // In the upper bytes of R's bits the keys of a wavefront mostly share
     // one digit: then one lane adds them all (one LDS atomic, not one per key
     // on the same counter); otherwise every key adds itself.
@@ -323,12 +337,39 @@ __device__ uint64_t radix_select(KeyAt key_at, int n, int k, uint32_t* hist, int
         for (int j = 3; j > 0 && above + hv[j] < uk; --j, --d) above += hv[j];
         *s_digit = d;
         *s_k = k - int(above);
+        sm->bucket = int(d == 4 * l + 3 ? h3 : d == 4 * l + 2 ? h2 : d == 4 * l + 1 ? h1 : h0);
       }
     }
     __syncthreads();
     prefix |= uint64_t(*s_digit) << shift;
     pmask |= uint64_t(255) << shift;
     k = *s_k;
+    if (shift > 0 && sm->bucket <= 64) {
+      // gather the bucket (prefix matched so far) and finish by counting
+      for (int i = tid; i < n; i += kK3Block) {
+        const uint64_t key = key_at(i);
+        if ((key & pmask) == prefix) sm->key[atomicAdd(&sm->n, 1)] = key;
+      }
+      __syncthreads();
+      if (tid < 64) {
+        const int m = sm->n;
+        const uint64_t mine = tid < m ? sm->key[tid] : 0;
+        int above = 0, not_below = 0;
+        for (int j = 0; j < m; ++j) {
+          const uint64_t kj = sm->key[j];
+          above += kj > mine ? 1 : 0;
+          not_below += kj >= mine ? 1 : 0;
+        }
+        // the k-th largest: fewer than k keys above it, at least k at or above
+        if (tid < m && above < k && not_below >= k) {
+          sm->T = mine;
+          sm->rest = k - above;
+        }
+      }
+      __syncthreads();
+      *rest = sm->rest;
+      return sm->T;
+    }
   }
   *rest = k;
   return prefix;
@@ -405,6 +446,7 @@ __device__ void select_body(const SelectArgs& a) {
   __shared__ int32_t c_idx[kCap];
   __shared__ int32_t tie_idx[kK3Block];
   __shared__ uint32_t hist[2 * 256];
+  __shared__ RadixSmall rsm;
   __shared__ int cnt[2];  // active, ties
   __shared__ int s_digit, s_k;
   uint32_t* scan = reinterpret_cast<uint32_t*>(tie_idx);  // the global path reuses it
@@ -493,7 +535,7 @@ __device__ void select_body(const SelectArgs& a) {
     int need = 0;
     const uint64_t* __restrict__ keys = a.keys;
     const uint64_t T = radix_select([=](int i) { return keys[i]; }, U, a.max_o, hist, &s_digit,
-                                    &s_k, &need);
+                                    &s_k, &need, &rsm);
     c_act = select_by_scan(a, T, need, scan);
   } else {
     for (int i = tid; i < n_cand; i += kK3Block) {
@@ -504,7 +546,7 @@ __device__ void select_body(const SelectArgs& a) {
     __syncthreads();
     int need = 0;
     const uint64_t T = radix_select([&](int i) { return c_key[i]; }, n_cand, a.max_o, hist,
-                                    &s_digit, &s_k, &need);
+                                    &s_digit, &s_k, &need, &rsm);
     // Ties at T: gather their indices; when more tie than may be taken, keep
     // the `need` smallest indices, i.e. every tie with index <= cut.
     for (int i = tid; i < n_cand; i += kK3Block) {

@@ -286,16 +286,18 @@ def test_abi_errors_leave_state_unchanged():
 
 
 @pytest.mark.parametrize("case", ["small_pool_ties_at_cut", "pool_at_count_limit",
-                                  "pool_over_count_limit", "few_ties_at_cut",
+                                  "pool_over_count_limit", "small_tie_in_radix", "few_ties_at_cut",
                                   "mid_pool_ties_at_cut", "many_ties_at_cut", "pool_at_capacity",
                                   "huge_pool"])
 def test_selection_paths(case):
     """Top_maxO through each selection path of the kernel: small pools (up
     to 128 candidates) ranked by direct counting, with index-ordered ties at
     the cut and at the size limit; larger pools by radix select in LDS, with
-    the ties at the cut sorted (few_ties_at_cut, mid_pool_ties_at_cut), with
-    more ties than the tie buffer, and right at the LDS pool's capacity
-    (12,288); more candidates than that over the global keys."""
+    the early finish on a small bucket holding a tie at the cut
+    (small_tie_in_radix), with larger ties at the cut sorted
+    (few_ties_at_cut, mid_pool_ties_at_cut), with more ties than the tie
+    buffer, and right at the LDS pool's capacity (12,288); more candidates
+    than that over the global keys."""
     torch = require_gpu()
     from paper_2606_00539_amd import Controller
 
@@ -316,6 +318,16 @@ def test_selection_paths(case):
         n = 128 if case == "pool_at_count_limit" else 129
         base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
         base[9, rng.permutation(U)[:n]] *= 6.0 + rng.random(n)
+    elif case == "small_tie_in_radix":
+        # 400 candidates: 40 distinct spikes, a 60-unit tie holding the cut (the
+        # radix select finishes early on a bucket of at most 64), 300 weaker
+        perm = rng.permutation(U)
+        base = np.exp(rng.normal(scale=0.01, size=(T, U)))   # no natural triggers
+        tied, strong, weak = perm[:60], perm[60:100], perm[100:400]
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+        base[9, strong] *= 18.0 + np.arange(40)
+        base[9, weak] *= 2.0 + 0.01 * rng.random(300)
     elif case == "few_ties_at_cut":
         # 300 units share one norm stream and spike together; 20 spike harder
         tied = rng.choice(U, 300, replace=False)
@@ -355,7 +367,8 @@ def test_selection_paths(case):
             assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} t={t}")
             if t == 10:
                 want = {"pool_at_capacity": 12288, "pool_at_count_limit": 128,
-                        "pool_over_count_limit": 129, "small_pool_ties_at_cut": 100}
+                        "pool_over_count_limit": 129, "small_pool_ties_at_cut": 100,
+                        "small_tie_in_radix": 400}
                 if case in want:
                     assert ref.stats["n_cand"] == want[case]
                 if case == "mid_pool_ties_at_cut":
