@@ -249,13 +249,43 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
   float ss = 0.0f;
   const int m_lane = m0 + wm * 128 + (lane & 31);
   const int n_lane = n0 + wn * 128 + 4 * (lane >> 5);
+  // Accumulating: the stored tile is first copied into the LDS buffers (free
+  // once the loop is done) by direct-to-LDS 16-byte loads, which need no
+  // registers: each wavefront instruction fills two rows of 512 B, and chunk
+  // c of row r sits in slot c ^ (r % 32) of its row, so that the epilogue's
+  // reads of 32 consecutive rows at one column spread over the banks.  Loads
+  // of rows or columns outside dw read dw[0] instead (never used).
+  uint16_t* const old_tile = &lds[0][0][0];
+  static_assert(kWgBM * kWgBN <= 2 * 2 * kStage, "the stored tile fits in the LDS buffers");
+  auto stage_old = [&]() {
+    __syncthreads();  // every wave is done with the operand buffers
+    const int row_in_pair = lane >> 5, slot = lane & 31;
+#pragma unroll 1
+    for (int q = 0; q < kWgBM / 2 / 4; ++q) {  // 32 row pairs per wave
+      const int row = (wave * (kWgBM / 8) + q) * 2 + row_in_pair;
+      const int m = m0 + row, n = n0 + 8 * (slot ^ (row & 31));
+      const uint16_t* src = (m < M && n < N) ? dw + int64_t(m) * N + n : dw;
+      __builtin_amdgcn_global_load_lds(
+          (const void*)src,
+          (__attribute__((address_space(3))) void*)(old_tile + (row & ~1) * kWgBN), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+  auto old_pair = [&](int m, int n) {  // the stored values at (m, n .. n+3)
+    const int row = m - m0, c = (n - n0) >> 3, w = (n - n0) & 7;
+    return *(const u32x2*)&old_tile[row * kWgBN + 8 * (c ^ (row & 31)) + w];
+  };
   auto epilogue = [&](auto accumulate) {
     constexpr bool kAcc = decltype(accumulate)::value;
+    if constexpr (kAcc) stage_old();
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = m_lane + 32 * i;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
+        // accumulating: keep each block's LDS reads next to their use
+        if constexpr (kAcc) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int n = n_lane + 32 * j + 8 * g;
@@ -264,7 +294,7 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
             float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1],
                   v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
             if constexpr (kAcc) {
-              const u32x2 old = *dst;
+              const u32x2 old = old_pair(m, n);
               v0 += bf16_val(old.x & 0xFFFFu);
               v1 += bf16_val(old.x >> 16);
               v2 += bf16_val(old.y & 0xFFFFu);
