@@ -111,9 +111,15 @@ def cpu_baseline_all_cores(buf, lay, w, single_gbs: float, target_s: float = 10.
         nbytes += n * esz
         if nbytes >= stage_bytes:
             break
-    sweeps = max(1, int(round(single_gbs * 1e9 * cores * target_s / nbytes)))
-    tasks = staged * sweeps
     with ThreadPoolExecutor(max_workers=cores) as pool:
+        # one untimed pilot sweep sizes the run: on small units the per-call
+        # overhead, not the bytes, sets the time
+        t0 = time.perf_counter()
+        list(pool.map(lambda seg: sumsq([seg]), staged))
+        pilot = time.perf_counter() - t0
+        sweeps = max(1, min(int(round(single_gbs * 1e9 * cores * target_s / nbytes)),
+                            int(target_s / max(pilot, 1e-6))))
+        tasks = staged * sweeps
         t0 = time.perf_counter()
         list(pool.map(lambda seg: sumsq([seg]), tasks))
         spent = time.perf_counter() - t0

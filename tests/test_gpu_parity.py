@@ -114,6 +114,53 @@ def test_sumsq_ragged_layouts(gen, misaligned):
             assert abs(got[b] - ref) <= 5e-6 * ref, (b, n, got[b], ref)
 
 
+@pytest.mark.parametrize("case", ["ragged_misaligned", "bf16_128_units"])
+def test_small_step_matches_norm_path(gen, case):
+    """A small workload's step (K1, then K2 and K3 in one workgroup) against
+    the same steps taken as K1 and the unit sums, then the controller from
+    those norms: every output bit-identical, step after step; the norms also
+    within the bar of the oracle's sum of squares."""
+    torch = require_gpu()
+    rng = np.random.default_rng(11)
+    if case == "ragged_misaligned":
+        lay, sizes, dtypes, pieces = ragged_layout(rng, True)
+    else:
+        sizes = [524289] + [524288] * 127                # 1 MiB of bf16 each, one ragged
+        dtypes = [V.DTYPE_BF16] * 128
+        pieces = [[n] for n in sizes]
+        lay = L.build(sizes, dtypes)
+    launches = 2
+    U = len(sizes)
+    say("small step vs norm path:", case, "units", U, "segments", lay.num_segments)
+    buf, base, ptrs = device_buffer(torch, lay)
+    cfg = dict(window=3, max_o=3, lock_len=2, eps=1e-12)
+    ss = torch.zeros(U, dtype=torch.float64, device="cuda")
+    with controller_for(lay, ptrs=ptrs, **cfg) as one, \
+            controller_for(lay, ptrs=ptrs, **cfg) as ref:
+        assert one.info()["launches_per_step"] == launches
+        scale = (10.0 ** rng.uniform(-4, -2, size=U)).astype(np.float32)
+        for t in range(1, 7):
+            step_scale = scale.copy()
+            step_scale[rng.choice(U, size=min(3, U), replace=False)] *= 20.0   # spikes
+            gen.fill(lay, base, 9, t, step_scale)
+            one.step(1.5, 1.3)
+            ref.sumsq(ss)
+            ref.step_from_norms(torch.sqrt(ss), 1.5, 1.3)
+            a, b = one.query(), ref.query()
+            for k in ("mask", "lock", "norm", "gnmr", "dgnmr", "risk"):
+                assert np.array_equal(a[k], b[k]), (case, t, k)
+            assert a["stats"] == b["stats"], (case, t)
+            assert a["stats"]["t"] == t
+            for u in range(U):
+                segs, start = [], 0
+                for m in pieces[u]:
+                    segs.append((V.unit_values(9, t, u, float(step_scale[u]), dtypes[u], start, m),
+                                 dtypes[u]))
+                    start += m
+                want = np.sqrt(oracle_sumsq(segs))
+                assert abs(a["norm"][u] - want) <= 1e-5 * want, (case, t, u, a["norm"][u], want)
+
+
 @pytest.mark.parametrize("name", ["tiny", "llama2-7b", "llama2-13b", "moe", "fine128", "fine32"])
 def test_logic_from_norms(name):
     """Alg. 1 + Alg. 2 on norm streams shaped like each workload: with identical
