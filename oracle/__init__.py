@@ -6,4 +6,4 @@ library or its binding and imports neither.
 """
 from .gnmr_oracle import (BF16, BUDGET_ACTIVE, BUDGET_ADMITTED, BUDGET_STATIC, F32,  # noqa: F401
                           Controller,
-                          StepResult, run_stream, sumsq, unit_norm, widen)
+                          StepResult, sumsq, unit_norm, widen)

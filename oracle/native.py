@@ -4,7 +4,6 @@ exact squares, float64 additions (here in index order)."""
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 import subprocess
 
@@ -48,7 +47,3 @@ def sumsq(values: np.ndarray, dtype: int) -> float:
         x = np.ascontiguousarray(values, dtype=np.uint16)
         return lib.oracle_sumsq_bf16(x.ctypes.data, x.size)
     raise ValueError(f"unknown dtype {dtype}")
-
-
-def unit_norm(segments) -> float:
-    return math.sqrt(sum(sumsq(v, d) for v, d in segments))
