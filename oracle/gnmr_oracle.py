@@ -34,7 +34,9 @@ Readings where the paper is silent:
   * t is the global controller step; every step is an observation, n = 0
     included.
   * Non-finite n (outside the paper): GNMR = D-GNMR = R = +inf, A_b kept,
-    1.0 pushed into Q_b, counted in n_nonfinite.
+    1.0 pushed into Q_b, counted in n_nonfinite.  A gradient whose sum of
+    squares reaches 2^128 (the end of the fp32 range the gradient pass
+    accumulates in) has norm +inf.
   * Statistics: n_trig_gnmr = #{GNMR/alpha > 1}, n_trig_dgnmr =
     #{D-GNMR/beta > 1}, n_trig = #{R > 1}, all over recoverable units;
     hit_maxo = 1 when the ranked pool is non-empty and at least maxO large.
@@ -97,8 +99,18 @@ def sumsq(segments, chunk: int = 1 << 22) -> float:
     return s
 
 
+# The gradient pass accumulates sums of squares in fp32, whose range ends at
+# 2^128.  Reading (non-finite norms are outside the paper): a unit whose sum
+# of squares reaches 2^128, i.e. whose norm is 2^64 or more, has a non-finite
+# norm, +inf.  NaN stays NaN.
+SUMSQ_LIMIT = 2.0 ** 128
+
+
 def unit_norm(segments) -> float:
-    return math.sqrt(sumsq(segments))
+    ss = sumsq(segments)
+    if ss >= SUMSQ_LIMIT:
+        return math.inf
+    return math.sqrt(ss)
 
 
 # --------------------------------------------------------------------------
@@ -300,11 +312,3 @@ class Controller:
         }
         return StepResult(t, n.copy(), gnmr, dgnmr, risk, mask, self.lock.astype(np.int32),
                           stats)
-
-
-def run_stream(norms_by_step, alphas, betas, **cfg) -> list[StepResult]:
-    """Run a controller over a [T, U] norm stream."""
-    norms_by_step = np.asarray(norms_by_step, dtype=np.float64)
-    ctl = Controller(norms_by_step.shape[1], **cfg)
-    return [ctl.step(norms_by_step[i], alphas[i], betas[i])
-            for i in range(norms_by_step.shape[0])]

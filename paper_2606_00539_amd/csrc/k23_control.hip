@@ -68,6 +68,16 @@ __global__ __launch_bounds__(256) void k_unit_sumsq(const int64_t* __restrict__ 
   if (lane == 0) out[b] = s;
 }
 
+// n_{b,t} from a unit's float64 sum of squares.  The sums of squares are
+// accumulated in fp32, whose range ends at 2^128: a unit whose sum reaches it
+// (a gradient norm of 2^64 or more) has no representable fp32 sum, so its
+// norm is taken as +inf, a non-finite norm (the outcome when an fp32 square
+// or partial overflows, made independent of how the sum is split into items).
+// NaN stays NaN.
+__device__ __forceinline__ double norm_of_sumsq(double ss) {
+  return ss >= 0x1p128 ? double(INFINITY) : sqrt(ss);
+}
+
 // Order-preserving key of a candidate: R >= 0 (or +inf), so its IEEE bits
 // are monotone in R; +1 keeps 0 free for "not a candidate".
 __device__ __forceinline__ uint64_t cand_key(double R) {
@@ -234,7 +244,7 @@ __global__ __launch_bounds__(256) void k2_update(UpdateArgs a) {
     if (a.ext_norm != nullptr) {
       n = a.ext_norm[b];
     } else {
-      n = sqrt(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
+      n = norm_of_sumsq(unit_ss<L>(a.unit_item_off, a.partial, b, lane, red));
     }
   }
   const bool has = in && lane == 0;
@@ -624,7 +634,7 @@ __global__ __launch_bounds__(kK3Block) void k23_small(UpdateArgs u, SelectArgs s
   if (has) {
     const double n = u.ext_norm != nullptr
                          ? u.ext_norm[b]
-                         : sqrt(unit_ss<1>(u.unit_item_off, u.partial, b, 0, nullptr));
+                         : norm_of_sumsq(unit_ss<1>(u.unit_item_off, u.partial, b, 0, nullptr));
     c = update_unit(u, b, n);
   }
   publish_local(s_counters, s_cand, has, b, c);

@@ -50,11 +50,17 @@ MUTANTS = [
     ("static mean over W+1 steps", "mean = self.gsum / W", "mean = self.gsum / (W + 1) - self.gsum * 0 + (np.arange(U) == 0)"),
     ("current GNMR in window", "for q in self.Q:                       # oldest to newest",
      "for q in self.Q[1:] + [gnmr]:"),
+    ("no sum-of-squares range limit", "if ss >= SUMSQ_LIMIT:", "if ss > SUMSQ_LIMIT * 4:"),
+    ("range limit on the norm, not its square", "if ss >= SUMSQ_LIMIT:",
+     "if ss >= 2.0 ** 64:"),
+    ("range limit strict", "if ss >= SUMSQ_LIMIT:", "if ss > SUMSQ_LIMIT:"),
 ]
 
 PINS = [
     (P.test_sumsq_matches_exact_rational, dict(dtype=P.BF16)),
     (P.test_norm_of_constant_magnitude_is_closed_form, {}),
+    (P.test_norm_range_ends_at_sum_of_squares_two_to_128, {}),
+    (P.test_norm_of_non_finite_elements, {}),
     (P.test_gnmr_and_dgnmr_follow_definitions, dict(delta=3)),
     (P.test_running_mean_is_arithmetic_mean, {}),
     (P.test_constant_magnitude_gives_exact_ones, {}),

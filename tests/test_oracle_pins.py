@@ -55,6 +55,47 @@ def test_norm_empty_unit_is_zero():
     assert unit_norm([(np.zeros(0, np.float32), F32)]) == 0.0
 
 
+def bf16_const(value, n):
+    return V.f32_to_bf16_bits(np.full(n, value, dtype=np.float32))
+
+
+def test_norm_range_ends_at_sum_of_squares_two_to_128():
+    # Reading for non-finite norms: the gradient pass accumulates in fp32, so
+    # a unit whose sum of squares reaches 2^128 has norm +inf.  Exact cases:
+    # two elements of 2^63 sum to 2^127 (norm 2^63.5), four to exactly 2^128.
+    assert unit_norm([(bf16_const(2.0 ** 63, 2), BF16)]) == 2.0 ** 63.5
+    assert unit_norm([(bf16_const(-(2.0 ** 63), 3), BF16)]) == np.sqrt(3.0) * 2.0 ** 63
+    assert unit_norm([(bf16_const(2.0 ** 63, 4), BF16)]) == np.inf
+    # one element of 2^64 (its square is 2^128), in a segment of small values
+    seg = bf16_const(2.0 ** -10, 1000)
+    seg[500] = bf16_const(-(2.0 ** 64), 1)[0]
+    assert unit_norm([(seg, BF16)]) == np.inf
+    # the largest bf16 below 2^64, alone: finite, exactly its magnitude
+    below = (2.0 - 2.0 ** -7) * 2.0 ** 63
+    assert unit_norm([(bf16_const(below, 1), BF16)]) == below
+    # split over segments, the limit applies to the unit's total
+    assert unit_norm([(bf16_const(2.0 ** 63, 2), BF16),
+                      (np.full(2, 2.0 ** 63, np.float32), F32)]) == np.inf
+    # fp32 values far beyond bf16's grid near the limit: 2^64 * (1 - 2^-24)
+    # squared is below 2^128; the sum of two such squares is not
+    v = np.float32(2.0 ** 64 * (1 - 2.0 ** -24))
+    assert unit_norm([(np.array([v], np.float32), F32)]) == float(v)
+    assert unit_norm([(np.array([v, v], np.float32), F32)]) == np.inf
+
+
+def test_norm_of_non_finite_elements():
+    # An Inf element gives an infinite sum of squares, a NaN element a NaN one
+    # (NaN wins over Inf), whatever the other elements are.
+    seg = bf16_const(2.0 ** -10, 64)
+    inf_seg = seg.copy()
+    inf_seg[3] = V.f32_to_bf16_bits(np.array([-np.inf], np.float32))[0]
+    assert unit_norm([(inf_seg, BF16)]) == np.inf
+    nan32 = np.full(9, 0.5, np.float32)
+    nan32[8] = np.nan
+    assert np.isnan(unit_norm([(nan32, F32)]))
+    assert np.isnan(unit_norm([(inf_seg, BF16), (nan32, F32)]))
+
+
 # --------------------------------------------------------------------------
 # GNMR and Delta-GNMR against the closed-form definitions (Sec. 3.1, 3.2)
 # --------------------------------------------------------------------------
