@@ -17,6 +17,9 @@
  *   - eps = 0 and a zero Delta-GNMR denominator give Delta-GNMR = 1.
  *   - A non-finite n_{b,t} (outside the paper): GNMR = Delta-GNMR = R = +inf,
  *     A_b is kept, 1.0 enters Q_b, and the unit is counted in n_nonfinite.
+ *     The gradient pass sums squares in fp32, whose range ends at 2^128: a
+ *     unit whose sum of squares reaches 2^128 (norm >= 2^64) gets n = +inf.
+ *     Inf or NaN gradient elements give n = +inf or NaN.
  *   - Units that are monitored but not recoverable get n, GNMR, Delta-GNMR
  *     and R, never enter C_t, and keep Lock = 0.
  *
@@ -110,9 +113,11 @@ typedef struct {
   int32_t reserved;
 } gnmr_stats;
 
-/* Create a controller: t = 0, A = 0, Q empty, Lock = 0 (the state before the
- * first step of Alg. 1 / Alg. 2).  Allocates all device state (O(U * delta)
- * doubles plus one float per 64 KiB work item) and builds the work list over
+/* Create a controller for the inputs of Alg. 1 (delta, eps) and Alg. 2
+ * (B_rec, maxO, T_lock) and the units of Sec. 3.4: t = 0, A = 0, Q empty,
+ * Lock = 0 (the state before the first step of Alg. 1 / Alg. 2).  Allocates
+ * all device state (O(U * delta) doubles plus one float per 64 KiB work
+ * item) and builds the work list over
  * the segments: each segment takes one item per started 64 KiB, at most
  * 16,777,215 items in all (the most one launch's grid can hold), and
  * seg_numel <= 2^50; GNMR_E_INVALID beyond.  `stream` orders the initial
@@ -124,8 +129,9 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg,
  * NULL is accepted and ignored. */
 gnmr_status gnmr_destroy(gnmr_ctx* ctx);
 
-/* One full controller step t -> t + 1 (Alg. 1 for every unit, then Alg. 2):
- * reads every gradient byte once, then updates A, Q, Lock and the outputs.
+/* One full controller step t -> t + 1: the gradient norm of every unit
+ * (Sec. 2), Alg. 1 for every unit, then Alg. 2: reads every gradient byte
+ * once, then updates A, Q, Lock and the outputs.
  * alpha_t, beta_t > 0 and finite (values below 1 are legal).  seg_ptr: host
  * [S] of device pointers for this step, or NULL to reuse the last bound ones.
  * Asynchronous: only enqueues work on `stream`.  The gradient buffers must
@@ -137,15 +143,18 @@ gnmr_status gnmr_destroy(gnmr_ctx* ctx);
 gnmr_status gnmr_step(gnmr_ctx* ctx, double alpha_t, double beta_t,
                       const void* const* seg_ptr, void* stream);
 
-/* The same step with the norms given: d_norm is device [num_units] float64
+/* Alg. 1 and Alg. 2 with the norms n_{b,t} given (the gradient norm of
+ * Sec. 2 computed by the caller): d_norm is device [num_units] float64
  * n_{b,t}; the gradient pass is skipped.  For callers that already hold the
  * norms (and for testing the state update and selection alone).  Capturable
  * in a HIP graph like gnmr_step. */
 gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm,
                                  double alpha_t, double beta_t, void* stream);
 
-/* The gradient pass alone, without touching controller state: writes
- * sum_i g_i^2 per unit (float64, device [num_units]) to d_sumsq.  seg_ptr as
+/* The gradient pass alone (Sec. 2, local-gradient equation, squared: the
+ * sum of squares over all of a unit's tensors), without touching controller
+ * state: writes sum_i g_i^2 per unit (float64, device [num_units]) to
+ * d_sumsq, the float64 sum of the fp32 item partials (no range limit applied).  seg_ptr as
  * in gnmr_step.  Asynchronous. */
 gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
                        double* d_sumsq, void* stream);
@@ -218,7 +227,9 @@ gnmr_status gnmr_bind_partials(gnmr_ctx* ctx, int64_t num_partials,
 gnmr_status gnmr_step_from_partials(gnmr_ctx* ctx, const float* d_partial,
                                     double alpha_t, double beta_t, void* stream);
 
-/* Copy the last step's outputs to host memory; every destination may be NULL.
+/* The outputs of Alg. 1 and Alg. 2 for the last step: A_t as a mask, the lock
+ * counters, n_{b,t}, GNMR, Delta-GNMR (Alg. 1) and R (Alg. 2), and the step's
+ * counters.  Copies them to host memory; every destination may be NULL.
  * Waits for `stream`.  Arrays are [num_units]: mask (1 = in A_t, recovery
  * path), lock (Lock_b after the step), norm (n_{b,t}), gnmr, dgnmr, risk (R).
  * GNMR_E_STATE before the first step. */
@@ -226,19 +237,23 @@ gnmr_status gnmr_query(gnmr_ctx* ctx, uint8_t* mask, int32_t* lock, double* norm
                        double* gnmr, double* dgnmr, double* risk,
                        gnmr_stats* stats, void* stream);
 
-/* Device addresses of the same outputs (owned by the context, valid until
- * gnmr_destroy, overwritten by the next step).  Any pointer may be NULL. */
+/* The same outputs of Alg. 1 and Alg. 2, zero-copy: their device addresses
+ * (owned by the context, valid until gnmr_destroy, overwritten by the next
+ * step; the mask can drive the actuator directly).  Any pointer may be NULL. */
 gnmr_status gnmr_device_outputs(gnmr_ctx* ctx, const uint8_t** mask,
                                 const int32_t** lock, const double** norm,
                                 const double** gnmr, const double** dgnmr,
                                 const double** risk, const gnmr_stats** stats);
 
-/* Controller state (t, A, Q, Lock, A_{t-1}, the static baseline's GNMR sums)
- * as a flat, versioned byte blob, for
- * checkpoint and resume.  gnmr_state_size gives the blob size; get copies it
- * to host `buf` of `bytes` >= that size (waits for `stream`); set restores a
- * blob taken from a context with the same num_units and window.  Restoring and
- * then stepping reproduces the original run bit for bit. */
+/* The state of Alg. 1 and Alg. 2 (t, A, Q, Lock; A_{t-1}; the static
+ * baseline's GNMR sums) as a flat, versioned byte blob, for checkpoint and
+ * resume (outside the paper: resume).  gnmr_state_size gives the blob size;
+ * get copies it to host `buf` of `bytes` >= that size (waits for `stream`);
+ * set restores a blob taken from a context with the same num_units, window,
+ * max_o, lock_len, eps, budget_mode and warmup_steps (GNMR_E_INVALID
+ * otherwise, nothing changed).  Restoring and then stepping reproduces the
+ * original run bit for bit.  The per-step outputs are not part of the state:
+ * after a restore gnmr_query returns GNMR_E_STATE until the next step. */
 gnmr_status gnmr_state_size(const gnmr_ctx* ctx, size_t* bytes);
 gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream);
 gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* stream);

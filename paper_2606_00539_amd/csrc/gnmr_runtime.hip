@@ -30,7 +30,7 @@ gnmr_status fail(gnmr_status st, const std::string& msg) {
   } while (0)
 
 constexpr uint32_t kStateMagic = 0x524D4E47u;  // "GNMR"
-constexpr uint32_t kStateVersion = 3;
+constexpr uint32_t kStateVersion = 4;
 constexpr int kProfileCapacity = 4096;
 
 struct StateHeader {
@@ -42,8 +42,10 @@ struct StateHeader {
   int32_t max_o;
   int32_t lock_len;
   double eps;
+  int32_t budget_mode;
+  int32_t warmup_steps;
 };
-static_assert(sizeof(StateHeader) == 40, "state header layout");
+static_assert(sizeof(StateHeader) == 48, "state header layout");
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -782,8 +784,8 @@ gnmr_status gnmr_get_state(gnmr_ctx* ctx, void* buf, size_t bytes, void* stream)
   int64_t t = 0;
   GNMR_HIP(hipMemcpyAsync(&t, ctx->d_step, sizeof(int64_t), hipMemcpyDeviceToHost, st));
   GNMR_HIP(hipStreamSynchronize(st));
-  StateHeader h{kStateMagic, kStateVersion, ctx->U, ctx->window, t,
-                ctx->max_o, ctx->lock_len, ctx->eps};
+  StateHeader h{kStateMagic, kStateVersion, ctx->U,        ctx->window,      t,
+                ctx->max_o,  ctx->lock_len,  ctx->eps, ctx->budget_mode, ctx->warmup_steps};
   char* p = static_cast<char*>(buf);
   memcpy(p, &h, sizeof h);
   p += sizeof h;
@@ -813,6 +815,14 @@ gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* s
     return fail(GNMR_E_INVALID, "not a GNMR state blob of this version");
   if (h.num_units != ctx->U || h.window != ctx->window)
     return fail(GNMR_E_INVALID, "state blob is for a different num_units or window");
+  // The blob's Lock values lie in [0, T_lock] and its queue, sums and A_{t-1}
+  // follow one budget convention: a context with other settings would step on
+  // from a state its own run could never reach.
+  if (h.max_o != ctx->max_o || h.lock_len != ctx->lock_len ||
+      h.eps != ctx->eps || h.budget_mode != ctx->budget_mode ||
+      h.warmup_steps != ctx->warmup_steps)
+    return fail(GNMR_E_INVALID,
+                "state blob is for different max_o, lock_len, eps, budget_mode or warmup_steps");
   if (h.t < 0) return fail(GNMR_E_INVALID, "state blob has a negative step counter");
   DeviceGuard g(ctx->device);
   if (!g.ok) return fail(GNMR_E_HIP, "cannot select the context's device");
@@ -830,6 +840,9 @@ gnmr_status gnmr_set_state(gnmr_ctx* ctx, const void* buf, size_t bytes, void* s
   p += U;
   GNMR_HIP(hipMemcpyAsync(ctx->d_gsum, p, U * sizeof(double), hipMemcpyHostToDevice, st));
   GNMR_HIP(hipMemcpyAsync(ctx->d_step, &h.t, sizeof(int64_t), hipMemcpyHostToDevice, st));
+  // The per-step outputs are not part of the state: clear the counters (t = 0)
+  // so that gnmr_query reports GNMR_E_STATE until the next step writes them.
+  GNMR_HIP(hipMemsetAsync(ctx->d_stats, 0, sizeof(gnmr_stats), st));
   GNMR_HIP(hipStreamSynchronize(st));
   return GNMR_OK;
 }
