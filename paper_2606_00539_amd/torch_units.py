@@ -20,6 +20,17 @@ from .binding import GNMR_BF16, GNMR_BUDGET_ACTIVE, GNMR_F32, Controller
 LLAMA_LINEARS = ("q_proj", "k_proj", "v_proj", "o_proj", "gate_proj", "up_proj", "down_proj")
 
 
+def _current(stream):
+    """`stream`, or torch's current stream when it is None: the stream that
+    backward wrote the gradients on and that K4 and K5 are launched on, so a
+    controller call is ordered after them also under `torch.cuda.stream(s)`."""
+    if stream is not None:
+        return stream
+    import torch
+
+    return torch.cuda.current_stream()
+
+
 def llama_linear_units(name: str):
     """Default unit map for LLaMA-style models: each attention / SwiGLU
     projection weight is one recoverable unit (Sec. 2 operator view); other
@@ -57,7 +68,7 @@ class TorchUnits:
         if recoverable is not None:
             rec = np.array([1 if recoverable(u) else 0 for u in self.unit_names], np.uint8)
         self.ctl = Controller(len(groups), window, max_o, lock_len, eps, off, numel, dtype,
-                              None, rec, stream, budget_mode, warmup_steps)
+                              None, rec, _current(stream), budget_mode, warmup_steps)
 
     def grad_pointers(self):
         ptrs = []
@@ -72,16 +83,16 @@ class TorchUnits:
 
     def step(self, alpha_t: float, beta_t: float, stream=None) -> None:
         """One controller step over the current gradients (asynchronous)."""
-        self.ctl.step(alpha_t, beta_t, seg_ptr=self.grad_pointers(), stream=stream)
+        self.ctl.step(alpha_t, beta_t, seg_ptr=self.grad_pointers(), stream=_current(stream))
 
     def query(self, stream=None) -> dict:
-        out = self.ctl.query(stream)
+        out = self.ctl.query(_current(stream))
         out["units"] = self.unit_names
         return out
 
     def recovery_set(self, stream=None) -> list:
         """Names of the units on the recovery path after the last step (A_t)."""
-        m = self.ctl.query(stream)["mask"]
+        m = self.ctl.query(_current(stream))["mask"]
         return [u for u, a in zip(self.unit_names, m) if a]
 
     def close(self):
@@ -186,7 +197,7 @@ class FusedWgradUnits:
         if recoverable is not None:
             rec = np.array([1 if recoverable(u) else 0 for u in self.unit_names], np.uint8)
         self.ctl = Controller(U, window, max_o, lock_len, eps, np.zeros(U + 1, np.int64), [], [],
-                              None, rec, stream, budget_mode, warmup_steps)
+                              None, rec, _current(stream), budget_mode, warmup_steps)
         self.ctl.bind_partials(self.part_off)
         self._produced = [None] * U   # data pointer of each layer's weight.grad
         self._saved_forward = []
@@ -234,16 +245,16 @@ class FusedWgradUnits:
                 raise RuntimeError(
                     f"{self.unit_names[b]}: weight.grad is not the gradient the fused backward "
                     "wrote since the last step (the layer did not run, or .grad was replaced)")
-        self.ctl.step_from_partials(self.partials, alpha_t, beta_t, stream)
+        self.ctl.step_from_partials(self.partials, alpha_t, beta_t, _current(stream))
         self._produced = [None] * len(self.modules)
 
     def query(self, stream=None) -> dict:
-        out = self.ctl.query(stream)
+        out = self.ctl.query(_current(stream))
         out["units"] = self.unit_names
         return out
 
     def recovery_set(self, stream=None) -> list:
-        m = self.ctl.query(stream)["mask"]
+        m = self.ctl.query(_current(stream))["mask"]
         return [u for u, a in zip(self.unit_names, m) if a]
 
     def close(self):
