@@ -19,6 +19,10 @@ Stored per workload:
                workloads of more than 400k unit-steps steps 1, 2 and every 16th
   sample       int64 [S] unit indices with float64 gnmr/dgnmr/risk [T, S]
 
+Policy variants (App. C budget remark, App. E.6 warm-up) are written under
+their own names (VARIANTS below) from the same stream, with the controller
+run under that policy; their files also hold budget_mode and warmup_steps.
+
 Usage: python tests/golden/make_e2e_golden.py [workload ...] [--threads N]
        python tests/golden/make_e2e_golden.py --thin workload ...   (rewrite an
        existing file with the norm subsampling above)
@@ -43,6 +47,15 @@ import streams as S  # noqa: E402
 from oracle import native  # noqa: E402
 from synth import host  # noqa: E402
 from synth import recipe as R  # noqa: E402
+
+from oracle import BUDGET_ACTIVE, BUDGET_ADMITTED  # noqa: E402
+
+# name -> (workload, budget_mode, warm-up steps): the admitted-only budget with
+# the high-fidelity warm-up over the first 5% of the steps (App. E.6), on the
+# MoE stream, whose pools of about 1,500 candidates make maxO = 32 bind.
+VARIANTS = {
+    "moe-admitted-warmup": ("moe", BUDGET_ADMITTED, math.ceil(0.05 * R.get("moe").steps)),
+}
 
 CHUNK = 1 << 22
 FULL_NORMS_MAX = 400_000      # unit-steps up to which every step's norms are kept
@@ -86,7 +99,8 @@ def unit_norm(seed, t, b, scale32, dtype, numel):
 
 
 def make(name: str, threads: int) -> str:
-    w = R.get(name)
+    base, budget_mode, warmup = VARIANTS.get(name, (name, BUDGET_ACTIVE, 0))
+    w = R.get(base)
     U, T = w.num_units, w.steps
     pool = ThreadPoolExecutor(max_workers=threads)
     t_start = time.time()
@@ -100,7 +114,8 @@ def make(name: str, threads: int) -> str:
             print(f"  {name} t={t}/{T} ({time.time() - t_start:.0f} s)", flush=True)
         return out
 
-    nudge, norms, res, _, _ = S.guarded_stream(w, norms_of_step)
+    nudge, norms, res, _, _ = S.guarded_stream(w, norms_of_step, budget_mode=budget_mode,
+                                               warmup_steps=warmup)
     pool.shutdown()
     masks = np.stack([r.mask for r in res]).astype(np.uint8)
     locks = np.stack([r.lock for r in res])
@@ -114,7 +129,7 @@ def make(name: str, threads: int) -> str:
     nt, nb = np.nonzero(nudge != 1.0)
     out = golden_path(name)
     np.savez_compressed(
-        out, workload=name, steps=T, units=U,
+        out, workload=base, budget_mode=budget_mode, warmup_steps=warmup, steps=T, units=U,
         nudge_t=(nt + 1).astype(np.int64), nudge_b=nb.astype(np.int64),
         nudge_f=nudge[nt, nb],
         mask_bits=np.packbits(masks, axis=1), lock=locks.astype(np.uint8), stats=stats,
@@ -135,6 +150,8 @@ def load(name: str) -> dict:
     d["mask"] = np.unpackbits(d["mask_bits"], axis=1, count=int(d["units"])).astype(np.uint8)
     if "norm_steps" not in d:
         d["norm_steps"] = np.arange(1, int(d["steps"]) + 1, dtype=np.int64)
+    d.setdefault("budget_mode", np.int64(BUDGET_ACTIVE))
+    d.setdefault("warmup_steps", np.int64(0))
     return d
 
 

@@ -7,9 +7,13 @@ no decision sits within that distance of its threshold.  On oracle values,
 every step must satisfy
   (G1) |GNMR/alpha - 1| > 1e-4, and |D-GNMR/beta - 1| > 1e-4 once the window
        is full, for every recoverable unit;
-  (G2) when |C_t| > maxO, the maxO-th and (maxO+1)-th largest R of C_t are
-       either exactly equal (a tie both sides compute identically, e.g. the
-       clamped value 1/beta) or at least 1e-4 apart relative.
+  (G2) when the ranked pool (C_t; C_t minus A_{t-1} under the admitted-only
+       budget; none in a warm-up step) holds more than maxO units, the
+       maxO-th and (maxO+1)-th largest R are either at least 1e-4 apart
+       relative, or exactly equal (a tie both sides compute identically, e.g.
+       the clamped value 1/beta) with the nearest distinct R above and below
+       the tied value at least 1e-4 away from it (so that no unit can move
+       across the tied group).
 A unit-step that breaks either is nudged: its fp32 scale is multiplied by
 (1 + 3e-4 j) for j = 1, -1, 2, -2, ... and the step is recomputed.
 """
@@ -17,7 +21,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from oracle import Controller, unit_norm
+from oracle import BUDGET_ACTIVE, BUDGET_ADMITTED, Controller, unit_norm
 from synth import values as V
 
 GUARD = 1e-4
@@ -43,8 +47,11 @@ def host_norms(w, t, scale32, units=None):
     return out
 
 
-def violations(res, alpha, beta, max_o, window_full, lock_before, rec=None):
-    """Units whose decisions break G1 or G2 at this step (oracle values)."""
+def violations(res, alpha, beta, max_o, window_full, lock_before, rec=None,
+               active_before=None, warm=False):
+    """Units whose decisions break G1 or G2 at this step (oracle values).
+    active_before: A_{t-1} when the admitted-only budget ranks only the new
+    candidates; warm: a warm-up step (no ranking)."""
     U = res.risk.size
     rec = np.ones(U, bool) if rec is None else rec
     bad = set()
@@ -53,13 +60,25 @@ def violations(res, alpha, beta, max_o, window_full, lock_before, rec=None):
     if window_full:
         d = res.dgnmr / beta
         bad |= set(np.flatnonzero(rec & np.isfinite(d) & (np.abs(d - 1.0) <= GUARD)).tolist())
+    if warm:
+        return sorted(bad)
     cand = rec & ((res.risk > 1.0) | (lock_before > 0))
+    if active_before is not None:
+        cand &= ~active_before
     idx = np.flatnonzero(cand)
     if 0 < max_o < idx.size:
         order = idx[np.lexsort((idx, -res.risk[idx]))]
         r_in, r_out = res.risk[order[max_o - 1]], res.risk[order[max_o]]
-        if r_in != r_out and (r_in - r_out) <= GUARD * r_in:
-            bad.add(int(order[max_o]))
+        if r_in != r_out:
+            if (r_in - r_out) <= GUARD * r_in:
+                bad.add(int(order[max_o]))
+        else:
+            r = res.risk[idx]
+            above, below = r[r > r_in], r[r < r_in]
+            if above.size and above.min() - r_in <= GUARD * above.min():
+                bad.add(int(idx[np.flatnonzero(r == above.min())[-1]]))
+            if below.size and r_in - below.max() <= GUARD * r_in:
+                bad.add(int(idx[np.flatnonzero(r == below.max())[0]]))
     return sorted(bad)
 
 
@@ -68,12 +87,16 @@ def nudge_factor(j: int) -> float:
     return 1.0 + (3e-4 * k if j % 2 == 1 else -3e-4 * k)
 
 
-def guarded_stream(w, norms_of_step, max_nudges: int = 40):
+def guarded_stream(w, norms_of_step, max_nudges: int = 40, budget_mode: int = BUDGET_ACTIVE,
+                   warmup_steps: int = 0):
     """Run the oracle over a workload's stream, nudging unit-steps that break
     the guards.  norms_of_step(t, scale32, units) -> {b: norm}.  Returns
     (nudge [T, U] float64, norms [T, U], results, alphas, betas)."""
+    if budget_mode not in (BUDGET_ACTIVE, BUDGET_ADMITTED):
+        raise ValueError("guards are defined for the active-set and admitted-only budgets")
     T, U = w.steps, w.num_units
-    ctl = Controller(U, window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=w.eps)
+    ctl = Controller(U, window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=w.eps,
+                     budget_mode=budget_mode, warmup_steps=warmup_steps)
     nudge = np.ones((T, U))
     norms = np.zeros((T, U))
     results, alphas, betas = [], [], []
@@ -87,7 +110,10 @@ def guarded_stream(w, norms_of_step, max_nudges: int = 40):
             snap = ctl.get_state()
             res = ctl.step(n, alpha, beta)
             bad = violations(res, alpha, beta, w.max_o, len(snap["Q"]) == w.window,
-                             snap["lock"])
+                             snap["lock"],
+                             active_before=(snap["active"] if budget_mode == BUDGET_ADMITTED
+                                            else None),
+                             warm=t <= warmup_steps)
             if not bad:
                 break
             ctl.set_state(snap)

@@ -6,7 +6,8 @@ gradients, the oracle's float64 norms and controller, and guard nudges that
 keep every decision at least 1e-4 from its threshold.  Here the same
 gradients are generated on the device (the HIP generator is bit-identical to
 the host twin) and run through gnmr_step in the benchmark's launch
-configuration.  Masks, locks and counters must match bit for bit at every
+configuration (the policy-variant files under the policy they were written
+with).  Masks, locks and counters must match bit for bit at every
 step; norms (all units, at the stored steps) and GNMR, Delta-GNMR and R (a
 stored sample of units, every step) within 1e-5.
 """
@@ -22,7 +23,8 @@ from synth import recipe as R
 
 pytestmark = pytest.mark.gpu
 
-E2E = ["tiny", "llama2-7b", "llama2-13b", "llama2-13b-layers", "moe", "fine128", "fine32"]
+E2E = ["tiny", "llama2-7b", "llama2-13b", "llama2-13b-layers", "moe", "fine128", "fine32",
+       "moe-admitted-warmup"]
 STAT_KEYS = ("t", "n_trig_gnmr", "n_trig_dgnmr", "n_trig", "n_cand", "n_active", "hit_maxo",
              "n_nonfinite")
 
@@ -39,18 +41,19 @@ def gen():
 def test_e2e_every_step_matches_oracle(gen, name):
     torch = require_gpu()
     d = load(name)
-    w = R.get(name)
+    w = R.get(str(d["workload"]))
+    policy = dict(budget_mode=int(d["budget_mode"]), warmup_steps=int(d["warmup_steps"]))
     assert int(d["units"]) == w.num_units and int(d["steps"]) == w.steps
     nudge = nudge_table(d)
     sample = d["sample"]
     lay = L.for_workload(w)
-    print(f"e2e {name}: {w.steps} steps x {w.num_units} units, "
+    print(f"e2e {name}: {w.steps} steps x {w.num_units} units, {policy}, "
           f"{len(d['nudge_t'])} nudged unit-steps ({golden_path(name)})", flush=True)
     sys.stdout.flush()
     buf, base, ptrs = device_buffer(torch, lay)
     active = 0
     try:
-        with controller_for(lay, w, ptrs) as ctl:
+        with controller_for(lay, w, ptrs, **policy) as ctl:
             for t in range(1, w.steps + 1):
                 gen.fill(lay, base, w.seed, t, w.scale32(t, nudge[t - 1]))
                 ctl.step(w.alpha(t), w.beta(t))
