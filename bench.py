@@ -36,6 +36,35 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# Worker threads of the all-cores leg: the CPU share that a one-GPU job has on
+# the GPU hosts this runs on is 16 threads, whatever the host's core count.
+CPU_SHARE_THREADS = 16
+
+
+def host_facts() -> dict:
+    """The host the CPU oracle ran on: logical CPUs, the affinity mask, the CPU
+    model and the BLAS thread pools NumPy would use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        import numpy  # noqa: F401  (loads the BLAS whose pools are listed)
+        from threadpoolctl import threadpool_info
+        blas = [{"api": i.get("internal_api"), "threads": i.get("num_threads")}
+                for i in threadpool_info()]
+    except Exception:                                  # pragma: no cover
+        pass
+    return {"os_cpu_count": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": model, "blas_pools_default": blas}
+
+
 def cpu_baseline(torch, buf, lay, w, target_s: float = 12.0, max_units: int = 100000):
     """Oracle norm pass plus one oracle controller step, single-threaded, on a
     bounded sample of units copied off the device (copy not timed)."""
@@ -74,7 +103,8 @@ def cpu_baseline(torch, buf, lay, w, target_s: float = 12.0, max_units: int = 10
     gbs = nbytes / spent / 1e9
     step_s = w.bytes_per_step / (nbytes / spent) + logic_s
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "us_per_step": round(step_s * 1e6, 1),
+            "us_per_step": round(step_s * 1e6, 1), "host": host_facts(),
+            "blas_threads_used": 1,
             "sample": f"float64 NumPy oracle norm pass over {units} of {w.num_units} units "
                       f"({nbytes / 1e9:.2f} GB, {spent:.1f} s) plus one oracle controller step "
                       f"over all units; us_per_step extrapolated to the full "
@@ -98,7 +128,7 @@ def cpu_baseline_all_cores(buf, lay, w, single_gbs: float, target_s: float = 10.
         limiter = threadpool_limits(limits=1)
     except Exception:                                  # pragma: no cover
         limiter = None
-    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    cores = max(1, min(CPU_SHARE_THREADS, len(os.sched_getaffinity(0))))
     order = np.random.default_rng(1).permutation(w.num_units)
     staged, nbytes = [], 0
     for b in order:
@@ -127,7 +157,9 @@ def cpu_baseline_all_cores(buf, lay, w, single_gbs: float, target_s: float = 10.
         limiter.unregister()
     total = nbytes * sweeps
     return {"value": round(total / spent / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle",
+            "kind": "oracle", "host": host_facts(), "blas_threads_used": 1,
+            "threads_rule": f"min(affinity CPUs, {CPU_SHARE_THREADS}): a one-GPU job's CPU "
+                            "share on these hosts",
             "sample": f"float64 NumPy oracle norm pass, {cores} threads over {len(staged)} "
                       f"units ({nbytes / 1e9:.2f} GB) swept {sweeps} times "
                       f"({total / 1e9:.1f} GB, {spent:.1f} s)"}
@@ -583,7 +615,13 @@ def main():
                               "eager steps; kernel times from HIP events in the same steps"
                               if in_region else
                               "eager steps (launch-bound: no events in them); kernel times "
-                              "from a second pass with HIP events")},
+                              "from a second pass with HIP events"),
+                   "timed_loop": "steady loop: the warm-up and timed steps all read one "
+                                 "resident buffer holding the stream's step-1 gradients "
+                                 "(every byte each step); after its first steps the candidate "
+                                 "pool is empty, so K3 does not rank. stream_step_us times every "
+                                 "step of the workload's own stream, with its real pools, right "
+                                 "after each step's gradients are generated"},
         "roofline": roofline,
         "step_us_spread": spread,
         "stream_step_us": stream_spread,
