@@ -159,6 +159,26 @@ gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm,
 gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
                        double* d_sumsq, void* stream);
 
+/* The gradient pass of gnmr_sumsq for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): no context, and no allocation, free or allocating
+ * library call.  The work list and the item partials live in a fixed device
+ * array of the library, GNMR_NOALLOC_SCRATCH_BYTES (32 MiB) per device, held
+ * from the first call on a device until the process ends.  segs describes the
+ * gradients as for gnmr_init, with seg_ptr required (host [S] of device
+ * pointers); the same checks apply.  Writes the same float64 sums of squares
+ * as gnmr_sumsq over the same layout, bit for bit, to d_sumsq (device
+ * [num_units]).  A layout whose work list and partials do not fit the array
+ * (about 1.5 million 64 KiB items, some 100 GB of gradients) is refused with
+ * GNMR_E_INVALID.  Enqueues an upload of the work list and two kernels on
+ * `stream`, then waits for `stream` (the host copy of the work list must
+ * outlive the upload).  All calls on one device share its array: calls that
+ * overlap (on different streams or threads) race; calls on one stream are
+ * ordered. */
+#define GNMR_NOALLOC_SCRATCH_BYTES (32u << 20)
+gnmr_status gnmr_sumsq_noalloc(int32_t num_units, const gnmr_segments* segs, double* d_sumsq,
+                               void* stream);
+
 /* ---- producer-fused gradient pass (the norm from the weight-gradient GEMM) --
  *
  * The controller takes one number per unit from the gradient: its norm

@@ -14,7 +14,7 @@ from .binding import (GNMR_BF16, GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED,  # no
                       gnmr_destroy, gnmr_device_outputs, gnmr_get_state, gnmr_info,
                       gnmr_init, gnmr_last_error, gnmr_profile_read, gnmr_query,
                       gnmr_set_profiling, gnmr_set_state, gnmr_state_size, gnmr_step,
-                      gnmr_step_from_norms, gnmr_sumsq, gnmr_wgrad_num_tiles,
+                      gnmr_step_from_norms, gnmr_sumsq, gnmr_sumsq_noalloc, gnmr_wgrad_num_tiles,
                       gnmr_wgrad_sumsq, gnmr_wgrad_sumsq_batched, gnmr_bind_partials, gnmr_step_from_partials,
                       load_library)
 from .schedule import two_stage_alpha  # noqa: F401

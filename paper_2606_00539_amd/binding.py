@@ -32,7 +32,8 @@ EXPORTED = ("gnmr_init", "gnmr_destroy", "gnmr_step", "gnmr_step_from_norms", "g
             "gnmr_last_error", "gnmr_actuator_create", "gnmr_actuate", "gnmr_actuator_info",
             "gnmr_actuator_destroy", "gnmr_wgrad_num_tiles", "gnmr_wgrad_sumsq",
             "gnmr_bind_partials", "gnmr_step_from_partials", "gnmr_wgrad_sumsq_batched",
-            "gnmr_actuate_matrix")
+            "gnmr_actuate_matrix", "gnmr_sumsq_noalloc")
+GNMR_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class GnmrError(RuntimeError):
@@ -112,6 +113,7 @@ def load_library(path: str = _LIB_PATH) -> ctypes.CDLL:
         "gnmr_bind_partials": [P, I64, P],
         "gnmr_wgrad_sumsq_batched": [P, I32, P, P],
         "gnmr_step_from_partials": [P, P, D, D, P],
+        "gnmr_sumsq_noalloc": [I32, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -187,6 +189,19 @@ def gnmr_sumsq(ctx, d_sumsq, seg_ptr=None, stream=None) -> None:
     p = d_sumsq.data_ptr() if hasattr(d_sumsq, "data_ptr") else int(d_sumsq)
     _check(load_library().gnmr_sumsq(ctx, None if ptrs is None else ctypes.cast(ptrs, ctypes.c_void_p),
                                      p, _stream(stream)))
+
+
+def gnmr_sumsq_noalloc(num_units, unit_seg_off, seg_numel, seg_dtype, seg_ptr, d_sumsq,
+                       stream=None) -> None:
+    uso = np.ascontiguousarray(unit_seg_off, dtype=np.int64)
+    numel = np.ascontiguousarray(seg_numel, dtype=np.int64)
+    dt = np.ascontiguousarray(seg_dtype, dtype=np.int32)
+    ptrs = None if seg_ptr is None else _ptr_array(seg_ptr)
+    segs = gnmr_segments(int(numel.size), uso.ctypes.data, numel.ctypes.data, dt.ctypes.data,
+                         None if ptrs is None else ctypes.cast(ptrs, ctypes.c_void_p))
+    p = d_sumsq.data_ptr() if hasattr(d_sumsq, "data_ptr") else int(d_sumsq)
+    _check(load_library().gnmr_sumsq_noalloc(int(num_units), ctypes.byref(segs), p,
+                                             _stream(stream)))
 
 
 def _dptr(p) -> int:

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <array>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -181,23 +182,82 @@ struct gnmr_ctx {
 
 namespace {
 
+// Checks a segment layout for U units: the CSR offsets, every segment's
+// size and dtype, and the K1 item count (one workgroup per item, and a grid
+// holds fewer than 2^32 lanes).
+gnmr_status check_layout(const gnmr_segments* segs, int64_t U) {
+  const int64_t S = segs->num_segments;
+  if (S < 0 || S > INT32_MAX) return fail(GNMR_E_INVALID, "num_segments out of range");
+  if (segs->unit_seg_off == nullptr) return fail(GNMR_E_INVALID, "unit_seg_off is NULL");
+  if (S > 0 && (segs->seg_numel == nullptr || segs->seg_dtype == nullptr))
+    return fail(GNMR_E_INVALID, "seg_numel or seg_dtype is NULL");
+  if (segs->unit_seg_off[0] != 0 || segs->unit_seg_off[U] != S)
+    return fail(GNMR_E_INVALID, "unit_seg_off must start at 0 and end at num_segments");
+  for (int64_t b = 0; b < U; ++b)
+    if (segs->unit_seg_off[b + 1] < segs->unit_seg_off[b])
+      return fail(GNMR_E_INVALID, "unit_seg_off must be non-decreasing");
+  const int64_t max_items = int64_t(UINT32_MAX) / gnmr::kK1Block;
+  int64_t num_items = 0;
+  for (int64_t s = 0; s < S; ++s) {
+    const int64_t n = segs->seg_numel[s];
+    if (n < 0) return fail(GNMR_E_INVALID, "negative seg_numel");
+    if (segs->seg_dtype[s] != GNMR_F32 && segs->seg_dtype[s] != GNMR_BF16)
+      return fail(GNMR_E_INVALID, "unknown seg_dtype " + std::to_string(segs->seg_dtype[s]));
+    const int64_t per = gnmr::kItemBytes / (segs->seg_dtype[s] == GNMR_BF16 ? 2 : 4);
+    if (n > (int64_t(1) << 50)) return fail(GNMR_E_INVALID, "seg_numel above 2^50");
+    num_items += (n + per - 1) / per;  // at most 2^37 more: no overflow before the test
+    if (num_items > max_items)
+      return fail(GNMR_E_INVALID, "too many work items for one launch: more than " +
+                                      std::to_string(max_items) +
+                                      " (each segment takes one item per started 64 KiB)");
+  }
+  return GNMR_OK;
+}
+
+// The K1 work list of a checked layout: each segment cut into items of
+// kItemBytes, in unit order; unit b owns items [unit_item_off[b],
+// unit_item_off[b+1]).  Returns the gradient bytes of one pass.
+int64_t build_work_list(const gnmr_segments* segs, int64_t U, std::vector<Item>* items,
+                        std::vector<int64_t>* unit_item_off) {
+  int64_t bytes = 0;
+  items->clear();
+  unit_item_off->assign(size_t(U) + 1, 0);
+  for (int64_t b = 0; b < U; ++b) {
+    for (int64_t s = segs->unit_seg_off[b]; s < segs->unit_seg_off[b + 1]; ++s) {
+      const int64_t n = segs->seg_numel[s];
+      const int64_t esz = segs->seg_dtype[s] == GNMR_BF16 ? 2 : 4;
+      const int64_t per = gnmr::kItemBytes / esz;
+      bytes += n * esz;
+      for (int64_t e0 = 0; e0 < n; e0 += per)
+        items->push_back(Item{e0, int32_t(s), int32_t(std::min(per, n - e0))});
+    }
+    (*unit_item_off)[size_t(b) + 1] = int64_t(items->size());
+  }
+  return bytes;
+}
+
 gnmr_status check_thresholds(double alpha, double beta) {
   if (!(alpha > 0.0) || !(beta > 0.0) || !isfinite(alpha) || !isfinite(beta))
     return fail(GNMR_E_INVALID, "alpha_t and beta_t must be finite and > 0");
   return GNMR_OK;
 }
 
-gnmr_status check_ptrs(const gnmr_ctx* c, const void* const* ptrs) {
-  for (int64_t s = 0; s < c->S; ++s) {
-    if (c->seg_numel[s] == 0) continue;
+gnmr_status check_seg_ptrs(int64_t S, const int64_t* numel, const int32_t* dtype,
+                           const void* const* ptrs) {
+  for (int64_t s = 0; s < S; ++s) {
+    if (numel[s] == 0) continue;
     const uintptr_t p = reinterpret_cast<uintptr_t>(ptrs[s]);
-    const uintptr_t esz = c->seg_dtype[s] == GNMR_BF16 ? 2 : 4;
+    const uintptr_t esz = dtype[s] == GNMR_BF16 ? 2 : 4;
     if (p == 0) return fail(GNMR_E_INVALID, "segment " + std::to_string(s) + ": NULL pointer");
     if (p % esz != 0)
       return fail(GNMR_E_INVALID,
                   "segment " + std::to_string(s) + ": pointer not aligned to its element size");
   }
   return GNMR_OK;
+}
+
+gnmr_status check_ptrs(const gnmr_ctx* c, const void* const* ptrs) {
+  return check_seg_ptrs(c->S, c->seg_numel.data(), c->seg_dtype.data(), ptrs);
 }
 
 // Copies this step's segment pointers to the device table on `st`.
@@ -344,31 +404,8 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
   if (cfg->budget_mode == GNMR_BUDGET_STATIC && cfg->warmup_steps < 1)
     return fail(GNMR_E_INVALID, "the static baseline needs warmup_steps >= 1");
   const int64_t U = cfg->num_units, S = segs->num_segments;
-  if (S < 0 || S > INT32_MAX) return fail(GNMR_E_INVALID, "num_segments out of range");
-  if (segs->unit_seg_off == nullptr) return fail(GNMR_E_INVALID, "unit_seg_off is NULL");
-  if (S > 0 && (segs->seg_numel == nullptr || segs->seg_dtype == nullptr))
-    return fail(GNMR_E_INVALID, "seg_numel or seg_dtype is NULL");
-  if (segs->unit_seg_off[0] != 0 || segs->unit_seg_off[U] != S)
-    return fail(GNMR_E_INVALID, "unit_seg_off must start at 0 and end at num_segments");
-  for (int64_t b = 0; b < U; ++b)
-    if (segs->unit_seg_off[b + 1] < segs->unit_seg_off[b])
-      return fail(GNMR_E_INVALID, "unit_seg_off must be non-decreasing");
-  // one K1 workgroup per item, and a grid holds fewer than 2^32 lanes
-  const int64_t max_items = int64_t(UINT32_MAX) / gnmr::kK1Block;
-  int64_t num_items = 0;
-  for (int64_t s = 0; s < S; ++s) {
-    const int64_t n = segs->seg_numel[s];
-    if (n < 0) return fail(GNMR_E_INVALID, "negative seg_numel");
-    if (segs->seg_dtype[s] != GNMR_F32 && segs->seg_dtype[s] != GNMR_BF16)
-      return fail(GNMR_E_INVALID, "unknown seg_dtype " + std::to_string(segs->seg_dtype[s]));
-    const int64_t per = gnmr::kItemBytes / (segs->seg_dtype[s] == GNMR_BF16 ? 2 : 4);
-    if (n > (int64_t(1) << 50)) return fail(GNMR_E_INVALID, "seg_numel above 2^50");
-    num_items += (n + per - 1) / per;  // at most 2^37 more: no overflow before the test
-    if (num_items > max_items)
-      return fail(GNMR_E_INVALID, "too many work items for one launch: more than " +
-                                      std::to_string(max_items) +
-                                      " (each segment takes one item per started 64 KiB)");
-  }
+  gnmr_status lr = check_layout(segs, U);
+  if (lr != GNMR_OK) return lr;
 
   // K2 workgroups of 1, 4 or 256 units fill counter set w % kCounterSets:
   // each set's share of the candidate list must fit its capacity
@@ -398,19 +435,9 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
     }
   }
 
-  // K1 work list: each segment cut into items of kItemBytes, in unit order.
   std::vector<Item> items;
-  std::vector<int64_t> unit_item_off(size_t(U) + 1, 0);
-  for (int64_t b = 0; b < U; ++b) {
-    for (int64_t s = segs->unit_seg_off[b]; s < segs->unit_seg_off[b + 1]; ++s) {
-      const int64_t esz = c->seg_dtype[s] == GNMR_BF16 ? 2 : 4;
-      const int64_t per = gnmr::kItemBytes / esz;
-      c->bytes_per_step += c->seg_numel[s] * esz;
-      for (int64_t e0 = 0; e0 < c->seg_numel[s]; e0 += per)
-        items.push_back(Item{e0, int32_t(s), int32_t(std::min(per, c->seg_numel[s] - e0))});
-    }
-    unit_item_off[size_t(b) + 1] = int64_t(items.size());
-  }
+  std::vector<int64_t> unit_item_off;
+  c->bytes_per_step = build_work_list(segs, U, &items, &unit_item_off);
   c->num_items = int64_t(items.size());
 
   // One device arena for all state.
@@ -723,6 +750,102 @@ gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr, double* d_sums
                               ctx->d_partial, st));
   GNMR_HIP(gnmr::launch_unit_sumsq(ctx->d_unit_item_off, ctx->d_partial, ctx->num_items,
                                    ctx->U, d_sumsq, st));
+  return GNMR_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The gradient pass without allocation: the work list and the item partials
+// live in `scratch`, a fixed device array of the library (each device holds
+// its own copy for the life of the process).  Host code reaches it only
+// through the address hipGetSymbolAddress gives on that device: the array's
+// name is not a device address in host code.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = GNMR_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device, looked up on the
+// first call there (with that device current) and kept.
+gnmr_status scratch_address(void** out) {
+  int dev = -1;
+  GNMR_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(GNMR_E_HIP, "device index " + std::to_string(dev) + " out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    GNMR_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr) return fail(GNMR_E_HIP, "hipGetSymbolAddress gave no address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GNMR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gnmr_status gnmr_sumsq_noalloc(int32_t num_units, const gnmr_segments* segs, double* d_sumsq,
+                               void* stream) {
+  if (num_units < 1) return fail(GNMR_E_INVALID, "num_units must be >= 1");
+  if (segs == nullptr) return fail(GNMR_E_INVALID, "segs is NULL");
+  if (d_sumsq == nullptr) return fail(GNMR_E_INVALID, "d_sumsq is NULL");
+  const int64_t U = num_units, S = segs->num_segments;
+  gnmr_status r = check_layout(segs, U);
+  if (r != GNMR_OK) return r;
+  if (S > 0 && segs->seg_ptr == nullptr)
+    return fail(GNMR_E_INVALID, "seg_ptr is NULL: this call binds no pointers beforehand");
+  r = check_seg_ptrs(S, segs->seg_numel, segs->seg_dtype, segs->seg_ptr);
+  if (r != GNMR_OK) return r;
+  std::vector<Item> items;
+  std::vector<int64_t> unit_item_off;
+  build_work_list(segs, U, &items, &unit_item_off);
+  const int64_t n_items = int64_t(items.size());
+  // scratch layout: item table, unit offsets, segment bases and dtypes (one
+  // upload), then the item partials
+  const size_t o_items = 0;
+  const size_t o_uoff = align_up(o_items + size_t(n_items) * sizeof(Item), 256);
+  const size_t o_base = align_up(o_uoff + (size_t(U) + 1) * sizeof(int64_t), 256);
+  const size_t o_dt = align_up(o_base + size_t(S) * sizeof(void*), 256);
+  const size_t o_part = align_up(o_dt + size_t(S) * sizeof(int32_t), 256);
+  const size_t total = o_part + size_t(n_items) * sizeof(float);
+  if (total > kScratchBytes)
+    return fail(GNMR_E_INVALID, "the layout needs " + std::to_string(total) +
+                                    " bytes of scratch (work list and partials); the "
+                                    "allocation-free pass holds " +
+                                    std::to_string(kScratchBytes));
+  void* sp = nullptr;
+  r = scratch_address(&sp);
+  if (r != GNMR_OK) return r;
+  std::vector<unsigned char> blob(o_part, 0);
+  memcpy(blob.data() + o_items, items.data(), size_t(n_items) * sizeof(Item));
+  memcpy(blob.data() + o_uoff, unit_item_off.data(), (size_t(U) + 1) * sizeof(int64_t));
+  if (S > 0) {
+    memcpy(blob.data() + o_base, segs->seg_ptr, size_t(S) * sizeof(void*));
+    memcpy(blob.data() + o_dt, segs->seg_dtype, size_t(S) * sizeof(int32_t));
+  }
+  char* base = static_cast<char*>(sp);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // ordered after earlier work on `stream`, so a previous call's kernels have
+  // read the old work list before it is replaced
+  GNMR_HIP(hipMemcpyAsync(base, blob.data(), blob.size(), hipMemcpyHostToDevice, st));
+  GNMR_HIP(gnmr::launch_sumsq(reinterpret_cast<const Item*>(base + o_items), n_items,
+                              reinterpret_cast<const char* const*>(base + o_base),
+                              reinterpret_cast<const int32_t*>(base + o_dt),
+                              reinterpret_cast<float*>(base + o_part), st));
+  GNMR_HIP(gnmr::launch_unit_sumsq(reinterpret_cast<const int64_t*>(base + o_uoff),
+                                   reinterpret_cast<const float*>(base + o_part), n_items,
+                                   num_units, d_sumsq, st));
+  // the host copy of the work list must outlive the upload
+  GNMR_HIP(hipStreamSynchronize(st));
   return GNMR_OK;
 }
 

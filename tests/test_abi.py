@@ -290,3 +290,28 @@ def test_fused_wgrad_units_rejects_unsupported_layers():
         FusedWgradUnits([("a", torch.nn.Linear(16, 16, bias=False))])
     with pytest.raises(ValueError):
         FusedWgradUnits([])
+
+
+def test_noalloc_sumsq_rejects_bad_arguments_before_the_device():
+    """gnmr_sumsq_noalloc checks the layout, the pointers and the scratch size
+    on the host; none of these calls reaches the device (the pointers are
+    never dereferenced)."""
+    from paper_2606_00539_amd import GnmrError, gnmr_sumsq_noalloc
+    from paper_2606_00539_amd import binding as B
+
+    out = 1 << 24
+    cases = [
+        (0, [0], [], [], [], out),                                  # no unit
+        (2, [0, 1, 1], [10], [B.GNMR_BF16], None, out),             # pointers required
+        (1, [0, 1], [10], [B.GNMR_BF16], [0], out),                 # NULL segment pointer
+        (1, [0, 1], [10], [B.GNMR_F32], [(1 << 20) + 2], out),      # misaligned fp32
+        (1, [0, 1], [10], [7], [1 << 20], out),                     # unknown dtype
+        (1, [0, 1], [10], [B.GNMR_BF16], [1 << 20], 0),             # no output
+        # 2^21 bf16 items: work list and partials beyond the 32 MiB scratch
+        (1, [0, 1], [(1 << 21) * 32768], [B.GNMR_BF16], [1 << 20], out),
+    ]
+    for U, off, numel, dt, ptrs, d_out in cases:
+        with pytest.raises(GnmrError) as e:
+            gnmr_sumsq_noalloc(U, off, numel, dt, ptrs, d_out)
+        assert e.value.status == B.GNMR_E_INVALID, (U, off, numel, dt, ptrs)
+    assert B.GNMR_NOALLOC_SCRATCH_BYTES == 32 << 20
