@@ -113,7 +113,10 @@ def _fused_linear_function():
         class FusedWgradLinear(torch.autograd.Function):
             @staticmethod
             def forward(ctx, x, weight, bias, units, index):
-                ctx.save_for_backward(x, weight)
+                spec = units._save_spec[index]
+                # the activation kept for the weight gradient: the input
+                # itself, or its per-token quantised copy (QuantizedSavedInputs)
+                ctx.save_for_backward(x if spec is None else _quantize_rows(x, spec), weight)
                 ctx.units, ctx.index = units, index
                 ctx.has_bias = bias is not None
                 # the same product as nn.Linear (bias fused: one rounding)
@@ -134,6 +137,23 @@ def _fused_linear_function():
 
         _FUNCTION = FusedWgradLinear
     return _FUNCTION
+
+
+def _quantize_rows(x, spec):
+    """The per-token fake quantisation of x (K4, gnmr_actuate_matrix) as a
+    new [tokens][features] bf16 tensor; spec = (device mask, unit, fmt_low,
+    fmt_recovery).  The mask entry is read when the kernel runs."""
+    import torch
+
+    from .binding import gnmr_actuate_matrix
+
+    d_mask, unit, fmt_low, fmt_recovery = spec
+    cols = x.shape[-1]
+    x2 = _kernel_operand(x, cols)
+    out = torch.empty_like(x2)
+    gnmr_actuate_matrix(x2, out, x2.shape[0], cols, d_mask, unit, fmt_low, fmt_recovery,
+                        torch.cuda.current_stream())
+    return out
 
 
 def _kernel_operand(t, features: int):
@@ -200,6 +220,7 @@ class FusedWgradUnits:
                               None, rec, _current(stream), budget_mode, warmup_steps)
         self.ctl.bind_partials(self.part_off)
         self._produced = [None] * U   # data pointer of each layer's weight.grad
+        self._save_spec = [None] * U  # per-token quantisation of the saved input, or None
         self._saved_forward = []
         for b, m in enumerate(self.modules):
             self._saved_forward.append(m.__dict__.get("forward"))
@@ -346,3 +367,104 @@ class QuantizedInputs:
         for h in self.handles:
             h.remove()
         self.handles = []
+
+
+_SAVED = None
+
+
+def _saved_quant_linear_function():
+    """The autograd function of a linear layer whose saved input is the
+    per-token quantised copy: the forward product uses the input itself, the
+    weight gradient the quantised copy."""
+    global _SAVED
+    if _SAVED is None:
+        import torch
+
+        class QuantSavedLinear(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, x, weight, bias, spec):
+                ctx.save_for_backward(_quantize_rows(x, spec), weight)
+                ctx.has_bias = bias is not None
+                # the same product as nn.Linear, on the unquantised input
+                return torch.nn.functional.linear(x, weight, bias)
+
+            @staticmethod
+            def backward(ctx, dy):
+                xq, weight = ctx.saved_tensors
+                dy2 = dy.reshape(-1, dy.shape[-1])
+                dx = torch.matmul(dy, weight) if ctx.needs_input_grad[0] else None
+                # dW = dy^T x_q, as nn.Linear's backward forms dy^T x
+                dw = dy2.t().mm(xq) if ctx.needs_input_grad[1] else None
+                db = dy2.sum(0) if ctx.has_bias and ctx.needs_input_grad[2] else None
+                return dx, dw, db, None
+
+        _SAVED = QuantSavedLinear
+    return _SAVED
+
+
+class QuantizedSavedInputs:
+    """The recovery actuator on saved activations only: the low-cost path of
+    the activation-quantisation stress bench (Sec. 5.1; App. E.2, recoverable
+    scope; App. E.4) quantises the activation a linear layer keeps for its
+    backward, not the input of its forward product.  Each listed layer
+    computes its output from its bf16 input unchanged; the copy it saves for
+    the weight gradient is fake-quantised per token (K4,
+    gnmr_actuate_matrix), in fmt_recovery when the layer's unit is in A_t and
+    in fmt_low otherwise, so dW = dy^T x_q while dx = dy W is exact in the
+    input.
+
+    `units` is a TorchUnits or a FusedWgradUnits; a module is actuated when
+    its name (as given in `named_modules`) is one of units.unit_names, and
+    follows that unit's entry of the controller's device mask, read when each
+    kernel runs (in stream order, no host synchronisation; before the first
+    step every unit is on the low-cost path).  With a FusedWgradUnits the
+    weight gradient and its tile sums come from K5 over the quantised copy;
+    otherwise the module's forward is routed through an autograd function
+    whose weight gradient is torch's product with the quantised copy.  The
+    modules must be bf16 nn.Linear layers whose input's last dimension is a
+    multiple of 8 in [8, 16384].  QuantizedInputs is the other reading: it
+    quantises the forward input itself.
+    """
+
+    def __init__(self, units, named_modules, fmt_low: int, fmt_recovery: int):
+        import torch
+
+        index = {n: b for b, n in enumerate(units.unit_names)}
+        self.units = units
+        self.d_mask = units.ctl.device_outputs()["mask"]
+        self.fmt_low, self.fmt_recovery = int(fmt_low), int(fmt_recovery)
+        self.fused = isinstance(units, FusedWgradUnits)
+        self.names, self._routed = [], []
+        for name, m in named_modules:
+            if name not in index:
+                continue
+            if m.weight.dtype != torch.bfloat16 or not m.weight.is_cuda:
+                raise TypeError(f"{name}: the weight must be a bf16 tensor on a HIP device")
+            spec = (self.d_mask, index[name], self.fmt_low, self.fmt_recovery)
+            if self.fused:
+                units._save_spec[index[name]] = spec
+            else:
+                self._routed.append((m, m.__dict__.get("forward")))
+                m.forward = self._routed_forward(m, spec)
+            self.names.append(name)
+        if not self.names:
+            raise ValueError("no module name matches a unit of the controller")
+
+    @staticmethod
+    def _routed_forward(m, spec):
+        fn = _saved_quant_linear_function()
+
+        def forward(x):
+            return fn.apply(x, m.weight, m.bias, spec)
+        return forward
+
+    def close(self):
+        if self.fused:
+            for name in self.names:
+                self.units._save_spec[self.units.unit_names.index(name)] = None
+        for m, f in self._routed:
+            if f is None:
+                m.__dict__.pop("forward", None)
+            else:
+                m.forward = f
+        self._routed, self.names = [], []
