@@ -468,3 +468,119 @@ class QuantizedSavedInputs:
             else:
                 m.forward = f
         self._routed, self.names = [], []
+
+
+_QSIM = None
+
+
+def _qsim_linear_function():
+    """The autograd function of the quantisation-simulated linear operator."""
+    global _QSIM
+    if _QSIM is None:
+        import torch
+
+        class QuantSimLinear(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, x, weight, spec, capture):
+                d_mask, unit, f_lo, b_lo, f_hi, b_hi = spec
+                fwd = (d_mask, unit, f_lo, f_hi)
+                x_q = _quantize_rows(x, fwd)                         # per token
+                w_q = _quantize_rows(weight, fwd)                    # per output channel
+                y = torch.nn.functional.linear(x_q, w_q)
+                y_q = _quantize_rows(y, fwd)                         # per token
+                ctx.save_for_backward(x_q, w_q)
+                ctx.spec, ctx.capture, ctx.x_shape = spec, capture, x.shape
+                if capture is not None:
+                    capture.update(x_q=x_q, w_q=w_q, y=y, y_q=y_q)
+                return y_q.view(*x.shape[:-1], weight.shape[0])
+
+            @staticmethod
+            def backward(ctx, dy):
+                x_q, w_q = ctx.saved_tensors
+                d_mask, unit, f_lo, b_lo, f_hi, b_hi = ctx.spec
+                bwd = (d_mask, unit, b_lo, b_hi)
+                dy_q = _quantize_rows(dy, bwd)                       # per token
+                dx_q = dw_q = None
+                if ctx.needs_input_grad[0]:
+                    dx = torch.matmul(dy_q, w_q)
+                    dx_q = _quantize_rows(dx, bwd).view(ctx.x_shape)
+                if ctx.needs_input_grad[1]:
+                    dw = dy_q.t().mm(x_q)
+                    dw_q = _quantize_rows(dw, bwd)                   # per output channel
+                if ctx.capture is not None:
+                    ctx.capture.update(dy=dy.reshape(-1, dy.shape[-1]).clone(), dy_q=dy_q,
+                                       dx_q=dx_q, dw_q=dw_q)
+                return dx_q, dw_q, None, None
+
+        _QSIM = QuantSimLinear
+    return _QSIM
+
+
+class QuantSimLinears:
+    """The quantisation-simulated low-precision linear operator of App. E.2
+    on bias-free bf16 `nn.Linear` layers, its formats switched per unit by
+    the controller: forward, the input x and the weight w are fake-quantised
+    before the product and the output y again; backward, the incoming
+    gradient dy is quantised, and the computed dx and dw are quantised before
+    they go on (dx to the previous layer, dw to the optimiser and the
+    controller).  Every quantisation is K4's per-row recipe
+    (gnmr_actuate_matrix): rows are tokens for x, y, dy and dx and output
+    channels for w and dw.  The products are library GEMMs on the quantised
+    bf16 tensors (fp32 accumulation).
+
+    `low` and `recovery` are (forward format, backward format) pairs: a unit
+    outside A_t uses `low` (the paper's 4-bit E2M1 or 6-bit E3M2), a unit in
+    A_t `recovery` (the paper's hybrid FP8: E4M3 forward, E5M2 backward).  The
+    controller's device mask is read when each kernel runs, so a training
+    step's forward and backward use the decision of the last controller step
+    in stream order.  `units` is a TorchUnits whose units include the listed
+    modules' weights (their .grad is the quantised dw); modules are matched
+    by name against units.unit_names.  With capture=True the tensors of each
+    module's last forward and backward are kept in self.captured[name].
+    """
+
+    def __init__(self, units, named_modules, low=(1, 1), recovery=(3, 4), capture=False):
+        import torch
+
+        if isinstance(units, FusedWgradUnits):
+            raise TypeError("the weight gradient is quantised after its product: use "
+                            "TorchUnits, whose gradient pass reads the quantised .grad")
+        index = {n: b for b, n in enumerate(units.unit_names)}
+        self.units = units
+        self.d_mask = units.ctl.device_outputs()["mask"]
+        self.low, self.recovery = tuple(int(f) for f in low), tuple(int(f) for f in recovery)
+        self.captured = {} if capture else None
+        self.names, self._routed = [], []
+        for name, m in named_modules:
+            if name not in index:
+                continue
+            if m.weight.dtype != torch.bfloat16 or not m.weight.is_cuda:
+                raise TypeError(f"{name}: the weight must be a bf16 tensor on a HIP device")
+            if getattr(m, "bias", None) is not None:
+                raise TypeError(f"{name}: the simulated operator is bias-free")
+            spec = (self.d_mask, index[name], self.low[0], self.low[1], self.recovery[0],
+                    self.recovery[1])
+            cap = None
+            if capture:
+                cap = self.captured.setdefault(name, {})
+            self._routed.append((m, m.__dict__.get("forward")))
+            m.forward = self._routed_forward(m, spec, cap)
+            self.names.append(name)
+        if not self.names:
+            raise ValueError("no module name matches a unit of the controller")
+
+    @staticmethod
+    def _routed_forward(m, spec, cap):
+        fn = _qsim_linear_function()
+
+        def forward(x):
+            return fn.apply(x, m.weight, spec, cap)
+        return forward
+
+    def close(self):
+        for m, f in self._routed:
+            if f is None:
+                m.__dict__.pop("forward", None)
+            else:
+                m.forward = f
+        self._routed, self.names = [], []
