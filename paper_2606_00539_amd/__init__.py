@@ -17,4 +17,3 @@ from .binding import (GNMR_BF16, GNMR_BUDGET_ACTIVE, GNMR_BUDGET_ADMITTED,  # no
                       gnmr_step_from_norms, gnmr_sumsq, gnmr_sumsq_noalloc, gnmr_wgrad_num_tiles,
                       gnmr_wgrad_sumsq, gnmr_wgrad_sumsq_batched, gnmr_bind_partials, gnmr_step_from_partials,
                       load_library)
-from .schedule import two_stage_alpha  # noqa: F401

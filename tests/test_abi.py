@@ -66,13 +66,6 @@ def test_init_rejects_bad_configuration(bad):
     assert B.gnmr_last_error() != ""
 
 
-def test_two_stage_schedule():
-    from paper_2606_00539_amd import two_stage_alpha
-
-    assert [two_stage_alpha(t, 256) for t in (1, 7, 8, 256)] == [1.5, 1.5, 1.1, 1.1]
-    assert two_stage_alpha(1, 16) == 1.5 and two_stage_alpha(2, 16) == 1.1
-
-
 @pytest.mark.parametrize("bad", [
     dict(cols=12), dict(cols=0), dict(cols=16392), dict(unit=5), dict(unit=-1), dict(rows=-1),
     dict(in_=8), dict(out=0),
