@@ -432,6 +432,82 @@ def wgrad_bench(torch, tokens: int, steps: int, warmup: int) -> None:
     unfused.close()
 
 
+def qsim_bench(torch, tokens: int, steps: int, warmup: int) -> None:
+    """The actuator inside a training step, on the seven projections of one
+    LLaMA-2-13B layer at `tokens` tokens: forward and backward of bf16
+    bias-free linear layers (a) as plain layers, (b) with their saved inputs
+    quantised per token (QuantizedSavedInputs, E2M1), (c) as the
+    quantisation-simulated operator (QuantSimLinears: x, w, y, dy, dx and dw
+    quantised, E2M1).  Every unit is on the low-cost path (mask 0), the
+    formats' most quantising case."""
+    import numpy as np
+
+    from paper_2606_00539_amd import GNMR_FMT_BF16, GNMR_FMT_E2M1
+    from paper_2606_00539_amd.torch_units import (QuantizedSavedInputs, QuantSimLinears,
+                                                  TorchUnits)
+
+    d, ffn = 5120, 13824
+    shapes = {"q_proj": (d, d), "k_proj": (d, d), "v_proj": (d, d), "o_proj": (d, d),
+              "gate_proj": (ffn, d), "up_proj": (ffn, d), "down_proj": (d, ffn)}
+    torch.manual_seed(0)
+    layers = torch.nn.ModuleDict({n: torch.nn.Linear(i, o, bias=False)
+                                  for n, (o, i) in shapes.items()}).to("cuda", torch.bfloat16)
+    xs = {n: torch.randn(tokens, i, device="cuda").to(torch.bfloat16).requires_grad_(True)
+          for n, (o, i) in shapes.items()}
+    dys = {n: torch.randn(tokens, o, device="cuda").to(torch.bfloat16) * 1e-3
+           for n, (o, i) in shapes.items()}
+    flops = sum(3 * 2.0 * tokens * o * i for o, i in shapes.values())
+
+    def layer_step(_):
+        for n in shapes:
+            y = layers[n](xs[n])
+            y.backward(dys[n])
+        layers.zero_grad(set_to_none=True)
+        for x in xs.values():
+            x.grad = None
+
+    def timed():
+        for k in range(warmup):
+            layer_step(k)
+        torch.cuda.synchronize()
+        return event_time(torch, lambda: layer_step(0), steps)
+
+    units = TorchUnits(layers.named_parameters(), max_o=1, lock_len=1,
+                       unit_of=lambda n: n.split(".")[0])
+    results = {"plain_bf16": timed()}
+    saved = QuantizedSavedInputs(units, list(layers.named_children()), GNMR_FMT_E2M1,
+                                 GNMR_FMT_BF16)
+    results["saved_activations_e2m1"] = timed()
+    saved.close()
+    op = QuantSimLinears(units, list(layers.named_children()), low=(GNMR_FMT_E2M1,) * 2,
+                         recovery=(3, 4))
+    results["qsim_operator_e2m1"] = timed()
+    op.close()
+    units.close()
+    base = results["plain_bf16"]
+    # bytes K4 moves per layer step: the operator quantises x, w, y, dy, dx and dw
+    # (read + write, bf16); the saved-activation path quantises x only
+    act_bytes = {"saved_activations_e2m1": sum(2 * 2 * tokens * i for o, i in shapes.values()),
+                 "qsim_operator_e2m1": sum(2 * 2 * (tokens * i + o * i + tokens * o) * 2
+                                           for o, i in shapes.values())}
+    print(json.dumps({
+        "metric": "actuator inside a training step: one LLaMA-2-13B layer's seven projections, "
+                  "forward + backward, ms (lower is better)",
+        "value": round(results["qsim_operator_e2m1"], 4), "unit": "ms", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(results["qsim_operator_e2m1"], 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"LLaMA-2-13B decoder layer projections (q, k, v, o 5120x5120; "
+                               f"gate, up 13824x5120; down 5120x13824), {tokens} tokens, bf16, "
+                               "every unit on the E2M1 low-cost path", "tokens": tokens,
+                   "gemm_flops_per_step": flops},
+        "cases_ms": {k: round(v, 4) for k, v in results.items()},
+        "overhead_vs_plain": {k: round(v / base - 1, 4) for k, v in results.items()
+                              if k != "plain_bf16"},
+        "k4_bytes_per_step": act_bytes,
+        "plain_tflops": round(flops / (base * 1e-3) / 1e12, 1)}), flush=True)
+
+
 def stream_steps(torch, np, w, lay, buf, ptrs, stream):
     """Every step of the workload's stream on a fresh controller, each timed
     by a pair of events right after its gradients were generated (the
@@ -474,6 +550,9 @@ def main():
     ap.add_argument("--wgrad", action="store_true",
                     help="measure the gradient pass fused into the weight-gradient GEMMs of "
                          "one LLaMA-2-13B layer against library GEMMs + gnmr_step")
+    ap.add_argument("--qsim", action="store_true",
+                    help="measure the actuator inside a training step (saved activations, the "
+                         "quantisation-simulated operator) against plain bf16 layers")
     ap.add_argument("--budget-mode", choices=sorted(BUDGET_MODES), default="active",
                     help="controller policy: the active-set cap (default), the admitted-only "
                          "budget, or the static baseline (ranked once after the warm-up)")
@@ -507,6 +586,9 @@ def main():
         return
     if args.wgrad:
         wgrad_bench(torch, args.tokens, args.steps, args.warmup)
+        return
+    if args.qsim:
+        qsim_bench(torch, args.tokens, args.steps, args.warmup)
         return
     w = R.get(args.workload)
     lay = L.for_workload(w)
