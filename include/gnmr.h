@@ -154,8 +154,8 @@ gnmr_status gnmr_step_from_norms(gnmr_ctx* ctx, const double* d_norm,
 /* The gradient pass alone (Sec. 2, local-gradient equation, squared: the
  * sum of squares over all of a unit's tensors), without touching controller
  * state: writes sum_i g_i^2 per unit (float64, device [num_units]) to
- * d_sumsq, the float64 sum of the fp32 item partials (no range limit applied).  seg_ptr as
- * in gnmr_step.  Asynchronous. */
+ * d_sumsq, the float64 sum of the fp32 item partials (no range limit
+ * applied).  seg_ptr as in gnmr_step.  Asynchronous. */
 gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
                        double* d_sumsq, void* stream);
 
@@ -169,7 +169,7 @@ gnmr_status gnmr_sumsq(gnmr_ctx* ctx, const void* const* seg_ptr,
  * pointers); the same checks apply.  Writes the same float64 sums of squares
  * as gnmr_sumsq over the same layout, bit for bit, to d_sumsq (device
  * [num_units]).  A layout whose work list and partials do not fit the array
- * (about 1.5 million 64 KiB items, some 100 GB of gradients) is refused with
+ * (about 1.6 million 64 KiB items, some 100 GB of gradients) is refused with
  * GNMR_E_INVALID.  Enqueues an upload of the work list and two kernels on
  * `stream`, then waits for `stream` (the host copy of the work list must
  * outlive the upload).  All calls on one device share its array: calls that
