@@ -52,6 +52,20 @@ int main(void) {
   EXPECT(gnmr_actuate_matrix(NULL, NULL, 0, 64, NULL, 0, GNMR_FMT_INT8, GNMR_FMT_BF16,
                              NULL) == GNMR_OK);     /* no rows: nothing to do */
   EXPECT(gnmr_actuate(NULL, NULL, GNMR_FMT_E2M1, GNMR_FMT_BF16, NULL) == GNMR_E_INVALID);
+  {  /* the allocation-free pass: refused in its host checks, before any device call */
+    int64_t uoff[2] = {0, 1}, numel[1] = {(int64_t)1 << 36};  /* 2^21 bf16 items: 40 MiB */
+    int32_t dt[1] = {GNMR_BF16};
+    const void* ptrs[1] = {(const void*)4096};
+    gnmr_segments big;
+    big.num_segments = 1; big.unit_seg_off = uoff; big.seg_numel = numel;
+    big.seg_dtype = dt; big.seg_ptr = ptrs;
+    EXPECT(GNMR_NOALLOC_SCRATCH_BYTES == 32u << 20);
+    EXPECT(gnmr_sumsq_noalloc(1, &big, (double*)8192, NULL) == GNMR_E_INVALID);
+    EXPECT(strstr(gnmr_last_error(), "scratch") != NULL);
+    big.seg_ptr = NULL;
+    EXPECT(gnmr_sumsq_noalloc(1, &big, (double*)8192, NULL) == GNMR_E_INVALID);
+    EXPECT(gnmr_sumsq_noalloc(0, &big, (double*)8192, NULL) == GNMR_E_INVALID);
+  }
   printf("sizes %d %d %d %d %d\n", (int)sizeof(gnmr_config), (int)sizeof(gnmr_segments),
          (int)sizeof(gnmr_stats), (int)sizeof(gnmr_wgrad_problem), (int)sizeof(gnmr_act_segment));
   return fails;
