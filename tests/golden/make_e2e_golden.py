@@ -18,6 +18,9 @@ Stored per workload:
                the 1e-5 bar) at the 1-based steps norm_steps: every step, or for
                workloads of more than 400k unit-steps steps 1, 2 and every 16th
   sample       int64 [S] unit indices with float64 gnmr/dgnmr/risk [T, S]
+  gnmr_all, dgnmr_all  float32 [len(norm_steps), U] GNMR and Delta-GNMR of every
+               unit at the norm steps (workloads of more than 300 units, whose
+               sample above is a subset)
 
 Policy variants (App. C budget remark, App. E.6 warm-up) are written under
 their own names (VARIANTS below) from the same stream, with the controller
@@ -137,7 +140,12 @@ def make(name: str, threads: int) -> str:
         norm32=norms[norm_steps_for(T, U) - 1].astype(np.float32), sample=sample,
         gnmr=np.stack([r.gnmr[sample] for r in res]),
         dgnmr=np.stack([r.dgnmr[sample] for r in res]),
-        risk=np.stack([r.risk[sample] for r in res]))
+        risk=np.stack([r.risk[sample] for r in res]),
+        **({} if U <= 300 else {
+            "gnmr_all": np.stack([res[t - 1].gnmr for t in norm_steps_for(T, U)]).astype(
+                np.float32),
+            "dgnmr_all": np.stack([res[t - 1].dgnmr for t in norm_steps_for(T, U)]).astype(
+                np.float32)}))
     print(f"{name}: {T} steps x {U} units, {len(nt)} nudged unit-steps, "
           f"{int(masks.sum())} active unit-steps, {time.time() - t_start:.0f} s -> {out}",
           flush=True)

@@ -8,8 +8,9 @@ gradients are generated on the device (the HIP generator is bit-identical to
 the host twin) and run through gnmr_step in the benchmark's launch
 configuration (the policy-variant files under the policy they were written
 with).  Masks, locks and counters must match bit for bit at every
-step; norms (all units, at the stored steps) and GNMR, Delta-GNMR and R (a
-stored sample of units, every step) within 1e-5.
+step; norms, GNMR, Delta-GNMR and R of every unit at the stored steps (every
+step, or steps 1, 2 and every 16th on the longest streams), and of a stored
+sample of units at every step, within 1e-5.
 """
 import sys
 
@@ -69,6 +70,17 @@ def test_e2e_every_step_matches_oracle(gen, name):
                 if rows.size:
                     np.testing.assert_allclose(out["norm"], d["norm32"][rows[0]], rtol=1e-5,
                                                atol=0, err_msg=f"{what} norm")
+                if rows.size and "gnmr_all" in d:
+                    # every unit's ratios at the stored steps; R = max(G/alpha, D/beta)
+                    g, dd = d["gnmr_all"][rows[0]], d["dgnmr_all"][rows[0]]
+                    np.testing.assert_allclose(out["gnmr"], g, rtol=1e-5, atol=0,
+                                               err_msg=f"{what} gnmr (all units)")
+                    np.testing.assert_allclose(out["dgnmr"], dd, rtol=1e-5, atol=0,
+                                               err_msg=f"{what} dgnmr (all units)")
+                    r = np.maximum(g.astype(np.float64) / w.alpha(t),
+                                   dd.astype(np.float64) / w.beta(t))
+                    np.testing.assert_allclose(out["risk"], r, rtol=1e-5, atol=0,
+                                               err_msg=f"{what} risk (all units)")
                 for f in ("gnmr", "dgnmr", "risk"):
                     np.testing.assert_allclose(out[f][sample], d[f][t - 1], rtol=1e-5, atol=0,
                                                err_msg=f"{what} {f}")
