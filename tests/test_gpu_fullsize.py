@@ -113,3 +113,41 @@ def test_fullsize_sampled(gen, name, steps):
         pool.shutdown()
         del buf
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,steps", [("llama2-13b", 6), ("moe", 4)])
+def test_fullsize_scale_invariance(gen, name, steps):
+    """GNMR is dimensionless (Sec. 3.1): with eps = 0, multiplying every value
+    of unit b by 2^m_b at every step scales its norm by exactly 2^m_b (the
+    squares, their fp32 and float64 sums and the square root all commute with
+    a power of two away from the range limits), so GNMR, Delta-GNMR, R, the
+    mask, the locks and the counters of every unit are bit-identical to the
+    unscaled run, and every norm is exactly 2^m_b times the unscaled one.  At
+    full size, in the benchmark's launch configuration, every unit."""
+    torch = require_gpu()
+    w = R.get(name)
+    lay = L.for_workload(w)
+    U = w.num_units
+    m = np.random.default_rng(3).integers(-8, 9, size=U)
+    say(f"scale invariance {name}: {U} units x {steps} steps, m in [{m.min()}, {m.max()}]")
+    buf, base, ptrs = device_buffer(torch, lay)
+    cfg = dict(window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=0.0)
+    try:
+        with controller_for(lay, ptrs=ptrs, **cfg) as plain, \
+                controller_for(lay, ptrs=ptrs, **cfg) as scaled:
+            for t in range(1, steps + 1):
+                s32 = w.scale32(t)
+                gen.fill(lay, base, w.seed, t, s32)
+                plain.step(w.alpha(t), w.beta(t))
+                a = plain.query()
+                gen.fill(lay, base, w.seed, t, (s32 * np.exp2(m)).astype(np.float32))
+                scaled.step(w.alpha(t), w.beta(t))
+                b = scaled.query()
+                what = f"{name} t={t}"
+                for f in ("mask", "lock", "gnmr", "dgnmr", "risk"):
+                    assert np.array_equal(a[f], b[f]), f"{what}: {f} differs"
+                assert a["stats"] == b["stats"], what
+                assert np.array_equal(b["norm"], a["norm"] * np.exp2(m)), f"{what}: norm"
+    finally:
+        del buf
+        torch.cuda.empty_cache()
