@@ -837,15 +837,20 @@ gnmr_status gnmr_sumsq_noalloc(int32_t num_units, const gnmr_segments* segs, dou
   // ordered after earlier work on `stream`, so a previous call's kernels have
   // read the old work list before it is replaced
   GNMR_HIP(hipMemcpyAsync(base, blob.data(), blob.size(), hipMemcpyHostToDevice, st));
-  GNMR_HIP(gnmr::launch_sumsq(reinterpret_cast<const Item*>(base + o_items), n_items,
-                              reinterpret_cast<const char* const*>(base + o_base),
-                              reinterpret_cast<const int32_t*>(base + o_dt),
-                              reinterpret_cast<float*>(base + o_part), st));
-  GNMR_HIP(gnmr::launch_unit_sumsq(reinterpret_cast<const int64_t*>(base + o_uoff),
-                                   reinterpret_cast<const float*>(base + o_part), n_items,
-                                   num_units, d_sumsq, st));
-  // the host copy of the work list must outlive the upload
-  GNMR_HIP(hipStreamSynchronize(st));
+  hipError_t e = gnmr::launch_sumsq(reinterpret_cast<const Item*>(base + o_items), n_items,
+                                    reinterpret_cast<const char* const*>(base + o_base),
+                                    reinterpret_cast<const int32_t*>(base + o_dt),
+                                    reinterpret_cast<float*>(base + o_part), st);
+  if (e == hipSuccess)
+    e = gnmr::launch_unit_sumsq(reinterpret_cast<const int64_t*>(base + o_uoff),
+                                reinterpret_cast<const float*>(base + o_part), n_items,
+                                num_units, d_sumsq, st);
+  // the host copy of the work list must outlive the upload, also when a
+  // launch failed after it was enqueued
+  const hipError_t es = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(GNMR_E_HIP, std::string("launch: ") + hipGetErrorString(e));
+  if (es != hipSuccess)
+    return fail(GNMR_E_HIP, std::string("hipStreamSynchronize: ") + hipGetErrorString(es));
   return GNMR_OK;
 }
 
