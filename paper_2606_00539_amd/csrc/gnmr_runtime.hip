@@ -545,7 +545,10 @@ gnmr_status gnmr_init(gnmr_ctx** out, const gnmr_config* cfg, const gnmr_segment
                        size_t(gnmr::kCounterSets) * gnmr::kNumCounters * sizeof(int32_t), st);
   if (e == hipSuccess && S > 0)
     e = hipMemsetAsync(c->d_seg_base, 0, size_t(S) * sizeof(void*), st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  // wait for what was enqueued also on failure: the uploads read host vectors
+  // of this call and write the arena that bail() frees
+  const hipError_t es = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = es;
   if (e != hipSuccess) return bail(GNMR_E_HIP, std::string("init upload: ") + hipGetErrorString(e));
 
   if (segs->seg_ptr != nullptr) {
