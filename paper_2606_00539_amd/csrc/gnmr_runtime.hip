@@ -1129,7 +1129,9 @@ gnmr_status gnmr_actuator_create(gnmr_actuator** out, const gnmr_act_segment* se
   if (e == hipSuccess && !dsegs.empty())
     e = hipMemcpyAsync(a->d_segs, dsegs.data(), dsegs.size() * sizeof(gnmr::ActSeg),
                        hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  // wait for what was enqueued also on failure, before the arena is freed
+  const hipError_t es = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = es;
   if (e != hipSuccess) {
     (void)hipFree(a->arena);
     delete a;
