@@ -122,8 +122,10 @@ def test_fullsize_scale_invariance(gen, name, steps):
     squares, their fp32 and float64 sums and the square root all commute with
     a power of two away from the range limits), so GNMR, Delta-GNMR, R, the
     mask, the locks and the counters of every unit are bit-identical to the
-    unscaled run, and every norm is exactly 2^m_b times the unscaled one.  At
-    full size, in the benchmark's launch configuration, every unit."""
+    unscaled run, and every norm is exactly 2^m_b times the unscaled one.  A
+    second context over the unscaled values gives bit-identical outputs
+    (fixed work items and reduction trees, no float atomics).  At full size,
+    in the benchmark's launch configuration, every unit."""
     torch = require_gpu()
     w = R.get(name)
     lay = L.for_workload(w)
@@ -134,12 +136,16 @@ def test_fullsize_scale_invariance(gen, name, steps):
     cfg = dict(window=w.window, max_o=w.max_o, lock_len=w.lock_len, eps=0.0)
     try:
         with controller_for(lay, ptrs=ptrs, **cfg) as plain, \
+                controller_for(lay, ptrs=ptrs, **cfg) as again, \
                 controller_for(lay, ptrs=ptrs, **cfg) as scaled:
             for t in range(1, steps + 1):
                 s32 = w.scale32(t)
                 gen.fill(lay, base, w.seed, t, s32)
                 plain.step(w.alpha(t), w.beta(t))
-                a = plain.query()
+                again.step(w.alpha(t), w.beta(t))
+                a, a2 = plain.query(), again.query()
+                for f in ("mask", "lock", "norm", "gnmr", "dgnmr", "risk"):
+                    assert np.array_equal(a[f], a2[f]), f"{name} t={t}: {f} not repeatable"
                 gen.fill(lay, base, w.seed, t, (s32 * np.exp2(m)).astype(np.float32))
                 scaled.step(w.alpha(t), w.beta(t))
                 b = scaled.query()
