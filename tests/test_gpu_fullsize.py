@@ -115,7 +115,8 @@ def test_fullsize_sampled(gen, name, steps):
         torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("name,steps", [("llama2-13b", 6), ("moe", 4)])
+@pytest.mark.parametrize("name,steps", [("llama2-13b", 6), ("moe", 4), ("fine32", 4),
+                                        ("llama2-13b-layers", 3)])
 def test_fullsize_scale_invariance(gen, name, steps):
     """GNMR is dimensionless (Sec. 3.1): with eps = 0, multiplying every value
     of unit b by 2^m_b at every step scales its norm by exactly 2^m_b (the
