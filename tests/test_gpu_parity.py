@@ -114,19 +114,25 @@ def test_sumsq_ragged_layouts(gen, misaligned):
             assert abs(got[b] - ref) <= 5e-6 * ref, (b, n, got[b], ref)
 
 
-@pytest.mark.parametrize("case", ["ragged_misaligned", "bf16_128_units"])
+@pytest.mark.parametrize("case", ["ragged_misaligned", "bf16_128_units", "bf16_1024_units"])
 def test_small_step_matches_norm_path(gen, case):
     """A small workload's step (K1, then K2 and K3 in one workgroup) against
     the same steps taken as K1 and the unit sums, then the controller from
     those norms: every output bit-identical, step after step; the norms also
-    within the bar of the oracle's sum of squares."""
+    within the bar of the oracle's sum of squares.  bf16_1024_units sits at
+    the single workgroup's limit: 1,024 units of one work item each."""
     torch = require_gpu()
     rng = np.random.default_rng(11)
     if case == "ragged_misaligned":
         lay, sizes, dtypes, pieces = ragged_layout(rng, True)
-    else:
+    elif case == "bf16_128_units":
         sizes = [524289] + [524288] * 127                # 1 MiB of bf16 each, one ragged
         dtypes = [V.DTYPE_BF16] * 128
+        pieces = [[n] for n in sizes]
+        lay = L.build(sizes, dtypes)
+    else:
+        sizes = [20001] + [20000] * 1023                 # 40 kB of bf16 each, one ragged
+        dtypes = [V.DTYPE_BF16] * 1024
         pieces = [[n] for n in sizes]
         lay = L.build(sizes, dtypes)
     launches = 2
@@ -151,7 +157,7 @@ def test_small_step_matches_norm_path(gen, case):
                 assert np.array_equal(a[k], b[k]), (case, t, k)
             assert a["stats"] == b["stats"], (case, t)
             assert a["stats"]["t"] == t
-            for u in range(U):
+            for u in (range(U) if U <= 128 else sorted({0, 1, U - 1, *range(0, U, 37)})):
                 segs, start = [], 0
                 for m in pieces[u]:
                     segs.append((V.unit_values(9, t, u, float(step_scale[u]), dtypes[u], start, m),
@@ -420,6 +426,51 @@ def test_selection_paths(case):
                     assert ref.stats["n_cand"] == want[case]
                 if case == "mid_pool_ties_at_cut":
                     assert 128 < ref.stats["n_cand"] <= 12288
+
+
+@pytest.mark.parametrize("U", [1024, 1025])
+@pytest.mark.parametrize("case", ["small_pool_ties_at_cut", "radix_ties_at_cut", "every_unit"])
+def test_single_workgroup_selection_at_its_limit(U, case):
+    """The selection inside the single-workgroup kernel (K2 and K3 in one
+    launch, used up to 1,024 units) at its size limit, and one unit past it
+    (K2, then K3): a pool of 100 with a 60-unit tie at the cut (direct
+    counting), a pool of 700 with a 90-unit tie at the cut (radix select in
+    LDS), and every unit a candidate (alpha = 0.4); the oracle's decisions
+    bit for bit."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import Controller
+
+    rng = np.random.default_rng(U + len(case))
+    T, max_o, alpha = 12, 64, 1.1
+    base = np.exp(rng.normal(scale=0.01, size=(T, U)))       # no natural triggers
+    perm = rng.permutation(U)
+    if case == "small_pool_ties_at_cut":
+        tied, strong, weak = perm[:60], perm[60:80], perm[80:100]
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+        base[9, strong] *= 18.0 + np.arange(20)
+        base[9, weak] *= 2.0
+    elif case == "radix_ties_at_cut":
+        tied, strong, weak = perm[:90], perm[90:130], perm[130:700]
+        base[:, tied] = base[:, tied[:1]]
+        base[9, tied] *= 6.0
+        base[9, strong] *= 18.0 + np.arange(40)
+        base[9, weak] *= 2.0 + 0.01 * rng.random(570)
+    else:
+        alpha = 0.4                                          # |C_t| = U every step
+    ora = Oracle(U, window=5, max_o=max_o, lock_len=2, eps=1e-12)
+    dn = torch.empty(U, dtype=torch.float64, device="cuda")
+    say("single-workgroup selection:", case, "units", U)
+    with Controller(U, 5, max_o, 2, 1e-12, np.zeros(U + 1), [], []) as ctl:
+        for t in range(1, T + 1):
+            dn.copy_(torch.from_numpy(base[t - 1]))
+            ctl.step_from_norms(dn, alpha, 1.5)
+            ref = ora.step(base[t - 1], alpha, 1.5)
+            assert_step_matches(ctl.query(), ref, rtol=1e-14, what=f"{case} U={U} t={t}")
+            if t == 10 and case != "every_unit":
+                assert ref.stats["n_cand"] == (100 if case == "small_pool_ties_at_cut" else 700)
+            if case == "every_unit":
+                assert ref.stats["n_cand"] == U
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama2-13b", "moe", "fine32"])
