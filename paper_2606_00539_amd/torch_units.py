@@ -148,6 +148,10 @@ def _quantize_rows(x, spec):
     from .binding import gnmr_actuate_matrix
 
     d_mask, unit, fmt_low, fmt_recovery = spec
+    if x.dtype != torch.bfloat16 or not x.is_cuda:
+        # the kernel reads bf16 rows: any other element type would be misread
+        raise TypeError(f"per-token quantisation needs a bf16 tensor on a HIP device, got "
+                        f"{x.dtype} on {x.device}")
     cols = x.shape[-1]
     x2 = _kernel_operand(x, cols)
     out = torch.empty_like(x2)

@@ -285,6 +285,20 @@ def test_fused_wgrad_units_rejects_unsupported_layers():
         FusedWgradUnits([])
 
 
+def test_per_token_quantisation_refuses_other_element_types():
+    # the kernel reads bf16 rows: an fp32 or host tensor is refused before any
+    # library call (an fp32 buffer would otherwise be misread as bf16)
+    import torch
+
+    from paper_2606_00539_amd.torch_units import _quantize_rows
+
+    spec = (1 << 20, 0, 1, 3)               # never dereferenced
+    with pytest.raises(TypeError, match="bf16"):
+        _quantize_rows(torch.zeros(4, 16, dtype=torch.float32), spec)
+    with pytest.raises(TypeError, match="HIP device"):
+        _quantize_rows(torch.zeros(4, 16, dtype=torch.bfloat16), spec)
+
+
 def test_noalloc_sumsq_rejects_bad_arguments_before_the_device():
     """gnmr_sumsq_noalloc checks the layout, the pointers and the scratch size
     on the host; none of these calls reaches the device (the pointers are
