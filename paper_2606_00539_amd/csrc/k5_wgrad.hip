@@ -29,7 +29,6 @@
 // that the reads of the next buffer overlap it.  x is the matrix cores' A
 // operand, so the four accumulator rows a lane holds per group are four
 // consecutive output columns: each lane stores 8 contiguous bytes.
-#include <type_traits>
 
 #include "gnmr_internal.h"
 
@@ -58,11 +57,13 @@ constexpr int kSchedVmemRead = 0x020;
 constexpr int kSchedDsRead = 0x100;
 constexpr int kSchedDsWrite = 0x200;
 
-// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t to_bf16(float v) {
-  const uint32_t u = __float_as_uint(v);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to packed bf16 (lo in the low half), round to nearest
+// even, a NaN to a quiet NaN with its payload kept: one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 __device__ __forceinline__ float bf16_val(uint32_t b) { return __uint_as_float(b << 16); }
@@ -73,6 +74,9 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* p0, const uint16_t* p1) {
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// kAcc: every problem of the batch accumulates into its stored dw (true) or
+// overwrites it (false); a batch of both kinds takes one launch of each.
+template <bool kAcc>
 __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kStage];  // [stage][x, dy]
   __shared__ float red[kWgThreads / 64];
@@ -276,16 +280,17 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
     const int row = m - m0, c = (n - n0) >> 3, w = (n - n0) & 7;
     return *(const u32x2*)&old_tile[row * kWgBN + 8 * (c ^ (row & 31)) + w];
   };
-  auto epilogue = [&](auto accumulate) {
-    constexpr bool kAcc = decltype(accumulate)::value;
+  auto epilogue = [&]() {
     if constexpr (kAcc) stage_old();
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = m_lane + 32 * i;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        // accumulating: keep each block's LDS reads next to their use
-        if constexpr (kAcc) __builtin_amdgcn_sched_barrier(0);
+        // one block at a time: its conversions and stores (and, accumulating,
+        // its LDS reads) stay next to their use, which keeps the epilogue
+        // within the registers the accumulators leave free
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int n = n_lane + 32 * j + 8 * g;
@@ -300,24 +305,20 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
               v2 += bf16_val(old.y & 0xFFFFu);
               v3 += bf16_val(old.y >> 16);
             }
-            const uint32_t b0 = to_bf16(v0), b1 = to_bf16(v1), b2 = to_bf16(v2),
-                           b3 = to_bf16(v3);
-            const float q0 = bf16_val(b0), q1 = bf16_val(b1), q2 = bf16_val(b2),
-                        q3 = bf16_val(b3);
+            const uint32_t p01 = pack_bf16(v0, v1), p23 = pack_bf16(v2, v3);
+            const float q0 = __uint_as_float(p01 << 16), q1 = __uint_as_float(p01 & 0xFFFF0000u),
+                        q2 = __uint_as_float(p23 << 16), q3 = __uint_as_float(p23 & 0xFFFF0000u);
             ss = fmaf(q0, q0, ss);
             ss = fmaf(q1, q1, ss);
             ss = fmaf(q2, q2, ss);
             ss = fmaf(q3, q3, ss);
-            *dst = u32x2{b0 | (b1 << 16), b2 | (b3 << 16)};
+            *dst = u32x2{p01, p23};
           }
         }
       }
     }
   };
-  if (P.accumulate != 0)
-    epilogue(std::integral_constant<bool, true>{});
-  else
-    epilogue(std::integral_constant<bool, false>{});
+  epilogue();
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) ss += __shfl_xor(ss, d, 64);
   if (lane == 0) red[wave] = ss;
@@ -332,9 +333,27 @@ int64_t wgrad_tiles(int32_t M, int32_t N) {
 }
 
 hipError_t launch_wgrad(const WgBatch& batch, hipStream_t s) {
-  if (batch.total_tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(k5_wgrad, dim3(unsigned(batch.total_tiles)), dim3(kWgThreads), 0, s, batch);
-  return hipGetLastError();
+  // one launch per epilogue kind: the problems that overwrite dw, then those
+  // that accumulate into it, each launch with its own tile order
+  for (const int acc : {0, 1}) {
+    WgBatch b{};
+    for (int i = 0; i < batch.num; ++i) {
+      if ((batch.p[i].accumulate != 0) != (acc != 0)) continue;
+      WgProblem P = batch.p[i];
+      P.tile_begin = b.total_tiles;
+      b.total_tiles += P.tiles_m * P.tiles_n;
+      b.p[b.num++] = P;
+    }
+    if (b.total_tiles == 0) continue;
+    if (acc)
+      hipLaunchKernelGGL(k5_wgrad<true>, dim3(unsigned(b.total_tiles)), dim3(kWgThreads), 0, s, b);
+    else
+      hipLaunchKernelGGL(k5_wgrad<false>, dim3(unsigned(b.total_tiles)), dim3(kWgThreads), 0, s,
+                         b);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace gnmr
