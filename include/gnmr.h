@@ -216,7 +216,9 @@ gnmr_status gnmr_wgrad_sumsq(const void* dy, const void* x, void* dw, int64_t to
  * gnmr_wgrad_sumsq applies to each problem (and accumulate is 0 or 1,
  * reserved 0); across the batch no dw may overlap another problem's dw, dy
  * or x, or tile_sumsq (operands may be shared between problems: the seven
- * projections read three inputs).  Nothing is launched if a check fails. */
+ * projections read three inputs).  Nothing is launched if a check fails.
+ * The overwriting and the accumulating problems of a batch run as separate
+ * launches (one kernel instance per kind), in that order. */
 typedef struct {
   const void* dy;        /* device [tokens][out_features] bf16 */
   const void* x;         /* device [tokens][in_features] bf16  */
