@@ -41,6 +41,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(1))) u32x2 g_vec2;
+typedef __attribute__((address_space(1))) u32x4 g_vec4;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 // Buffer resource word 3 for gfx9-family raw (untyped) buffers.
@@ -280,40 +281,75 @@ __global__ __launch_bounds__(kWgThreads) void k5_wgrad(const WgBatch batch) {
     const int row = m - m0, c = (n - n0) >> 3, w = (n - n0) & 7;
     return *(const u32x2*)&old_tile[row * kWgBN + 8 * (c ^ (row & 31)) + w];
   };
+  // Rounds one group of four accumulator values (row m, columns n .. n+3)
+  // and adds their squares to ss in a fixed order; returns them packed.
+  auto round_group = [&](int i, int j, int g, int m, int n) {
+    float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1], v2 = acc[i][j][4 * g + 2],
+          v3 = acc[i][j][4 * g + 3];
+    if constexpr (kAcc) {
+      const u32x2 old = old_pair(m, n);
+      v0 += bf16_val(old.x & 0xFFFFu);
+      v1 += bf16_val(old.x >> 16);
+      v2 += bf16_val(old.y & 0xFFFFu);
+      v3 += bf16_val(old.y >> 16);
+    }
+    const uint32_t p01 = pack_bf16(v0, v1), p23 = pack_bf16(v2, v3);
+    const float q0 = __uint_as_float(p01 << 16), q1 = __uint_as_float(p01 & 0xFFFF0000u),
+                q2 = __uint_as_float(p23 << 16), q3 = __uint_as_float(p23 & 0xFFFF0000u);
+    ss = fmaf(q0, q0, ss);
+    ss = fmaf(q1, q1, ss);
+    ss = fmaf(q2, q2, ss);
+    ss = fmaf(q3, q3, ss);
+    return u32x2{p01, p23};
+  };
   auto epilogue = [&]() {
     if constexpr (kAcc) stage_old();
+    if (!kAcc && m0 + kWgBM <= M && n0 + kWgBN <= N) {
+      // Overwriting a tile wholly inside dw (uniform): the rounded tile goes
+      // to the free LDS buffers first, in the swizzled layout of the stored
+      // tile, then leaves in full rows: each wavefront store covers two whole
+      // 512-byte rows, where a lane's own accumulator layout would touch 32
+      // rows with 16 bytes each.  (Accumulating, the same staging spills
+      // registers and measured no faster, so those tiles store directly.)
+      __syncthreads();  // every wave is done with the operand buffers
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          // one block at a time: its conversions and LDS accesses stay next
+          // to their use, within the registers the accumulators leave free
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int m = m_lane + 32 * i, n = n_lane + 32 * j + 8 * g;
+            const u32x2 v = round_group(i, j, g, m, n);
+            const int row = m - m0, c = (n - n0) >> 3, w = (n - n0) & 7;
+            *(u32x2*)&old_tile[row * kWgBN + 8 * (c ^ (row & 31)) + w] = v;
+          }
+        }
+      }
+      __syncthreads();
+      const int c = tid & 31;
+      int row = tid >> 5;
+      uint16_t* out = dw + int64_t(m0 + row) * N + n0 + 8 * c;
+#pragma unroll 4
+      for (int p = 0; p < kWgBM * kWgBN / 8 / kWgThreads; ++p) {
+        *(g_vec4*)out = *(const u32x4*)&old_tile[row * kWgBN + 8 * (c ^ (row & 31))];
+        row += kWgThreads / 32;
+        out += int64_t(kWgThreads / 32) * N;
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = m_lane + 32 * i;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        // one block at a time: its conversions and stores (and, accumulating,
-        // its LDS reads) stay next to their use, which keeps the epilogue
-        // within the registers the accumulators leave free
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int n = n_lane + 32 * j + 8 * g;
-          if (m < M && n < N) {
-            g_vec2* dst = (g_vec2*)(dw + int64_t(m) * N + n);
-            float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1],
-                  v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-            if constexpr (kAcc) {
-              const u32x2 old = old_pair(m, n);
-              v0 += bf16_val(old.x & 0xFFFFu);
-              v1 += bf16_val(old.x >> 16);
-              v2 += bf16_val(old.y & 0xFFFFu);
-              v3 += bf16_val(old.y >> 16);
-            }
-            const uint32_t p01 = pack_bf16(v0, v1), p23 = pack_bf16(v2, v3);
-            const float q0 = __uint_as_float(p01 << 16), q1 = __uint_as_float(p01 & 0xFFFF0000u),
-                        q2 = __uint_as_float(p23 << 16), q3 = __uint_as_float(p23 & 0xFFFF0000u);
-            ss = fmaf(q0, q0, ss);
-            ss = fmaf(q1, q1, ss);
-            ss = fmaf(q2, q2, ss);
-            ss = fmaf(q3, q3, ss);
-            *dst = u32x2{p01, p23};
-          }
+          if (m < M && n < N) *(g_vec2*)(dw + int64_t(m) * N + n) = round_group(i, j, g, m, n);
         }
       }
     }
