@@ -28,7 +28,9 @@
 // one barrier per step, placed before the last slot's matrix-core work so
 // that the reads of the next buffer overlap it.  x is the matrix cores' A
 // operand, so the four accumulator rows a lane holds per group are four
-// consecutive output columns: each lane stores 8 contiguous bytes.
+// consecutive output columns, 8 contiguous bytes once rounded.  Overwritten
+// tiles that lie wholly inside dw pass through LDS and leave as full rows;
+// the others store each lane's 8 bytes directly.
 
 #include "gnmr_internal.h"
 
