@@ -21,6 +21,12 @@ Stored per workload:
   gnmr_all, dgnmr_all  float32 [len(norm_steps), U] GNMR and Delta-GNMR of every
                unit at the norm steps (workloads of more than 300 units, whose
                sample above is a subset)
+  rot_period, rot_norm32, rot_gnmr32, rot_dgnmr32, rot_risk32  (workloads of
+               more than 300 units) the norm, GNMR, Delta-GNMR and R of a
+               rotating set of units at every step: at step t the units
+               u = (t - 1) % P, (t - 1) % P + P, ... with P = rot_period, laid end
+               to end in step order, so that every step checks about U / P units
+               and every unit is checked at about T / P steps
 
 Policy variants (App. C budget remark, App. E.6 warm-up) are written under
 their own names (VARIANTS below) from the same stream, with the controller
@@ -62,6 +68,7 @@ VARIANTS = {
 
 CHUNK = 1 << 22
 FULL_NORMS_MAX = 400_000      # unit-steps up to which every step's norms are kept
+ROT_UNITS = 700               # units per step of the rotating set (about)
 STAT_KEYS = ("t", "n_trig_gnmr", "n_trig_dgnmr", "n_trig", "n_cand", "n_active", "hit_maxo",
              "n_nonfinite")
 
@@ -74,6 +81,16 @@ def norm_steps_for(steps: int, units: int) -> np.ndarray:
     if steps * units <= FULL_NORMS_MAX:
         return np.arange(1, steps + 1, dtype=np.int64)
     return np.array([t for t in range(1, steps + 1) if t <= 2 or t % 16 == 0], dtype=np.int64)
+
+
+def rot_period(units: int) -> int:
+    return -(-units // ROT_UNITS)
+
+
+def rot_units(t: int, units: int) -> np.ndarray:
+    """The rotating set of units whose outputs are stored at 1-based step t."""
+    p = rot_period(units)
+    return np.arange((t - 1) % p, units, p, dtype=np.int64)
 
 
 def thin(name: str) -> str:
@@ -145,7 +162,13 @@ def make(name: str, threads: int) -> str:
             "gnmr_all": np.stack([res[t - 1].gnmr for t in norm_steps_for(T, U)]).astype(
                 np.float32),
             "dgnmr_all": np.stack([res[t - 1].dgnmr for t in norm_steps_for(T, U)]).astype(
-                np.float32)}))
+                np.float32),
+            "rot_period": np.int64(rot_period(U)),
+            "rot_norm32": np.concatenate([norms[t - 1][rot_units(t, U)]
+                                          for t in range(1, T + 1)]).astype(np.float32),
+            **{f"rot_{f}32": np.concatenate([getattr(res[t - 1], f)[rot_units(t, U)]
+                                             for t in range(1, T + 1)]).astype(np.float32)
+               for f in ("gnmr", "dgnmr", "risk")}}))
     print(f"{name}: {T} steps x {U} units, {len(nt)} nudged unit-steps, "
           f"{int(masks.sum())} active unit-steps, {time.time() - t_start:.0f} s -> {out}",
           flush=True)

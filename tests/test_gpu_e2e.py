@@ -9,15 +9,17 @@ the host twin) and run through gnmr_step in the benchmark's launch
 configuration (the policy-variant files under the policy they were written
 with).  Masks, locks and counters must match bit for bit at every
 step; norms, GNMR, Delta-GNMR and R of every unit at the stored steps (every
-step, or steps 1, 2 and every 16th on the longest streams), and of a stored
-sample of units at every step, within 1e-5.
+step, or steps 1, 2 and every 16th on the longest streams), of a stored
+sample of units at every step, and (workloads of more than 300 units) of a
+rotating set of about 700 units at every step that visits every unit, within
+1e-5.
 """
 import sys
 
 import numpy as np
 import pytest
 
-from golden.make_e2e_golden import golden_path, load, nudge_table
+from golden.make_e2e_golden import golden_path, load, nudge_table, rot_units
 from gpu_util import controller_for, device_buffer, require_gpu
 from synth import layout as L
 from synth import recipe as R
@@ -53,6 +55,7 @@ def test_e2e_every_step_matches_oracle(gen, name):
     sys.stdout.flush()
     buf, base, ptrs = device_buffer(torch, lay)
     active = 0
+    rot_at = 0  # offset of this step's rotating set in the rot_* arrays
     try:
         with controller_for(lay, w, ptrs, **policy) as ctl:
             for t in range(1, w.steps + 1):
@@ -84,6 +87,15 @@ def test_e2e_every_step_matches_oracle(gen, name):
                 for f in ("gnmr", "dgnmr", "risk"):
                     np.testing.assert_allclose(out[f][sample], d[f][t - 1], rtol=1e-5, atol=0,
                                                err_msg=f"{what} {f}")
+                if "rot_period" in d:
+                    # the rotating set of units stored for this step
+                    ru = rot_units(t, w.num_units)
+                    sl = slice(rot_at, rot_at + ru.size)
+                    rot_at += ru.size
+                    for f, key in (("norm", "rot_norm32"), ("gnmr", "rot_gnmr32"),
+                                   ("dgnmr", "rot_dgnmr32"), ("risk", "rot_risk32")):
+                        np.testing.assert_allclose(out[f][ru], d[key][sl], rtol=1e-5, atol=0,
+                                                   err_msg=f"{what} {f} (rotating set)")
                 active += int(out["mask"].sum())
         print(f"  {name}: all {w.steps} steps match, {active} active unit-steps", flush=True)
     finally:
