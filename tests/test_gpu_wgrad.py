@@ -567,6 +567,41 @@ def test_accumulate_random_operands_within_bound_and_mixed_batch():
                                    atol=0, err_msg=f"problem {b}")
 
 
+@pytest.mark.parametrize("M,N", [(13824, 5120), (5120, 13824)])
+def test_accumulate_fullsize_sampled(M, N):
+    """accumulate = 1 at a 13B layer's full shapes and 4,096 tokens: a stored
+    gradient drawn on the host, then one micro-batch added by K5.  Sampled
+    elements against the oracle's float64 old + dy^T x within
+    error_bound_accumulate; sampled tile sums against float64 sums over the
+    stored result."""
+    torch = require_gpu()
+    from paper_2606_00539_amd import gnmr_wgrad_num_tiles, gnmr_wgrad_sumsq_batched
+
+    T = 4096
+    say(f"wgrad accumulate full size {M}x{N}, {T} tokens")
+    rng = np.random.default_rng(M + 7 * N)
+    old = W.bf16_rne(rng.normal(scale=1e-3, size=(M, N)))
+    dy, x = SW.operands(29, 2, 0, tokens=T, out_f=M, in_f=N)
+    dw = to_dev(torch, old)
+    ss = torch.full((gnmr_wgrad_num_tiles(M, N),), float("nan"), device="cuda")
+    gnmr_wgrad_sumsq_batched([(to_dev(torch, dy), to_dev(torch, x), dw, T, M, N, 1)], ss)
+    torch.cuda.synchronize()
+    got = dw.cpu().numpy().view(np.uint16)
+    rows = rng.choice(M, 24, replace=False)
+    cols = rng.choice(N, 24, replace=False)
+    exact = W.wgrad_accumulate_exact(old[np.ix_(rows, cols)], dy[:, rows], x[:, cols])
+    bound = W.error_bound_accumulate(old[np.ix_(rows, cols)], dy[:, rows], x[:, cols], exact)
+    err = np.abs(W.widen_bf16(got[np.ix_(rows, cols)]) - exact)
+    assert np.all(err <= bound), f"{M}x{N}: accumulated dw outside the bound"
+    ts = ss.cpu().numpy()
+    tn = N // 256
+    for tile in rng.choice(ts.size, 6, replace=False):
+        a, c = divmod(int(tile), tn)
+        blk = got[a * 256:(a + 1) * 256, c * 256:(c + 1) * 256]
+        np.testing.assert_allclose(ts[tile], W.tile_sumsq(blk)[0], rtol=SS_RTOL, atol=0,
+                                   err_msg=f"{M}x{N} tile {tile}")
+
+
 def test_fused_wgrad_units_with_bias_and_unaligned_views():
     """A biased layer (bias gradient left to torch) fed a view that starts off
     a 16-byte boundary: the operand is copied to an aligned buffer, and dW,
